@@ -1,0 +1,249 @@
+"""Benchmark: cache-cold batched FFT throughput on one MI355X, plus the SAR chain.
+
+One step is one forward FFT of the N = 4096, batch 32768, complex FP32 batch
+(1 GiB in, 1 GiB out: the whole working set is eight times the 256 MiB
+Infinity Cache, so every step streams from HBM).  ``value`` is algorithmic
+bytes (one read and one write per point, Section IV eq. (1)) over the wall
+time of the K timed steps.  The JSON line also carries:
+
+  roofline      the FFT kernel's algorithmic bytes per launch over its average
+                duration (HIP events around the timed launches on the launch
+                stream), against the 8 TB/s HBM peak; ``traffic`` comes from the
+                committed rocprofv3 FETCH_SIZE/WRITE_SIZE measurement when it
+                was taken on the current kernel sources, else null;
+  cpu_baseline  the fp64 oracle timed on this host on a bounded sample of the
+                same workload;
+  breakdown     the other workloads (N = 1024 latency case, 8192, 16384, FP16
+                storage, and the 4096 x 4096 SAR image with FP32 and FP16
+                intermediates), each a median of cache-flushed samples.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "batched FFT GB/s and % HBM peak at N=4096/8192/16384 (cache-cold); SAR ms/image"
+WORKLOAD = "fft_n4096_b32768_fp32"
+HBM_PEAK_GBS = 8000.0
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_digest() -> str:
+    """sha256 over the kernel sources; a traffic measurement is valid only for it."""
+    csrc = os.path.join(ROOT, "paper_2609_32237_amd", "csrc")
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".hpp", ".h")):
+            h.update(name.encode())
+            h.update(open(os.path.join(csrc, name), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def gflops(n, batch, seconds):
+    return 5.0 * n * np.log2(n) * batch / seconds / 1e9
+
+
+class Flusher:
+    """Writes a 1 GiB buffer on the current stream: evicts the 256 MiB Infinity
+    Cache and every L2 before a cache-cold sample (Section III's cold runs)."""
+
+    def __init__(self, torch):
+        self.buf = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+
+    def __call__(self):
+        self.buf.fill_(1.0)
+
+
+def time_samples(torch, fn, flush, samples, warmup=2):
+    """Median and quartiles (ms) of single calls, each after a cache flush."""
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(samples)]
+    for _ in range(warmup):
+        flush()
+        fn()
+    for a, b in ev:
+        flush()
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    ms = np.array([a.elapsed_time(b) for a, b in ev])
+    return float(np.median(ms)), float(np.percentile(ms, 25)), float(np.percentile(ms, 75))
+
+
+def fft_breakdown(torch, api, flush, name, samples):
+    import workloads
+
+    w = workloads.FFT_WORKLOADS[name]
+    n, batch, storage = w["n"], w["batch"], w["storage"]
+    x = torch.from_numpy(workloads.fft_workload(name)).cuda()
+    out = torch.empty_like(x)
+    plan = api.Plan(n, batch, 1, n, 0 if storage == "fp32" else 1, -1)
+    med, q1, q3 = time_samples(torch, lambda: plan.execute(x, out), flush, samples)
+    plan.close()
+    bytes_ = 2 * n * batch * (8 if storage == "fp32" else 4)
+    del x, out
+    torch.cuda.empty_cache()
+    gbs = bytes_ / (med * 1e-3) / 1e9
+    return {"n": n, "batch": batch, "storage": storage, "ms_median": round(med, 5), "ms_iqr": [round(q1, 5), round(q3, 5)],
+            "GB/s": round(gbs, 1), "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+            "GFLOPS": round(gflops(n, batch, med * 1e-3), 1)}
+
+
+def sar_breakdown(torch, api, flush, inter, samples):
+    import workloads
+
+    sc = workloads.sar_scene()
+    raw = torch.from_numpy(sc.raw).cuda()
+    hr = torch.from_numpy(sc.range_ref).cuda()
+    ha = torch.from_numpy(sc.az_ref).cuda()
+    out = torch.empty_like(raw)
+    ws = torch.empty(api._lib.sar_workspace_bytes(4096, 4096, inter), dtype=torch.uint8, device="cuda")
+    fn = lambda: api.sar_form_image(raw, hr, ha, inter, out=out, workspace=ws)  # noqa: E731
+    med, q1, q3 = time_samples(torch, fn, flush, samples)
+    bpp = 32 if inter == 0 else 24  # raw read + intermediate write + read + image write
+    bytes_ = bpp * 4096 * 4096
+    gbs = bytes_ / (med * 1e-3) / 1e9
+    return {"image": "4096x4096", "intermediate": "fp32" if inter == 0 else "fp16", "ms_median": round(med, 5),
+            "ms_iqr": [round(q1, 5), round(q3, 5)], "algorithmic_bytes_per_point": bpp, "GB/s": round(gbs, 1),
+            "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)}
+
+
+def cpu_baseline(x_host, n, target_s=10.0):
+    """The fp64 oracle on a bounded sample of the workload, on this host's cores."""
+    import oracle
+
+    threads = oracle.default_threads()
+    probe = 256
+    t0 = time.perf_counter()
+    oracle.fft(x_host[:probe], nthreads=threads)
+    t_probe = time.perf_counter() - t0
+    count = int(min(x_host.shape[0], max(probe, probe * target_s / max(t_probe, 1e-6))))
+    sample = x_host[:count]
+    xs = sample.astype(np.complex128)  # widening is not timed
+    t0 = time.perf_counter()
+    oracle.fft_layout(xs, n, count, 1, n, -1, nthreads=threads)
+    dt = time.perf_counter() - t0
+    return {"value": round(16.0 * n * count / dt / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {count} of {x_host.shape[0]} transforms (N={n}, fp64 radix-2, {dt:.1f} s)"}
+
+
+def load_traffic(digest: str):
+    path = os.path.join(PROFILES, f"traffic_{WORKLOAD}.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("kernel_source_digest") != digest:
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--samples", type=int, default=11, help="cache-flushed samples per breakdown workload")
+    ap.add_argument("--no-breakdown", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calib", action="store_true",
+                    help="also run an in-place scale of a 1 GiB buffer (known traffic) for counter calibration")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on one GPU; --gpus must be 1",
+                          "note": "batched transforms shard by batch with no communication"}))
+        sys.exit(2)
+
+    import torch
+
+    import workloads
+    from paper_2609_32237_amd import torch_api as api
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    w = workloads.FFT_WORKLOADS[WORKLOAD]
+    n, batch = w["n"], w["batch"]
+    log(f"generating {WORKLOAD}")
+    x_host = workloads.fft_workload(WORKLOAD)
+    x = torch.from_numpy(x_host).cuda()
+    out = torch.empty_like(x)
+    plan = api.Plan(n, batch, 1, n, 0, -1)
+    step_bytes = 2 * 8 * n * batch
+
+    if args.copy_calib:
+        cal = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        for _ in range(3):
+            cal.mul_(1.0)
+        torch.cuda.synchronize()
+        del cal
+
+    for _ in range(args.warmup):
+        plan.execute(x, out)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    log(f"timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        plan.execute(x, out)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kernel_ms = e0.elapsed_time(e1) / args.steps
+    value = step_bytes * args.steps / wall / 1e9
+    achieved = step_bytes / (kernel_ms * 1e-3) / 1e9
+
+    digest = kernel_source_digest()
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": load_traffic(digest),
+                "kernel": "fft_kernel rows N=4096 fp32 forward", "algorithmic_bytes_per_launch": step_bytes,
+                "avg_launch_ms": round(kernel_ms, 5), "kernel_source_digest": digest}
+    result = {
+        "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(wall * 1e3 / args.steps, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": WORKLOAD, "n": n, "batch": batch, "storage": "fp32", "direction": "forward",
+                   "layout": "contiguous rows", "cache": "cold: 2 GiB working set vs 256 MiB Infinity Cache",
+                   "gflops_5nlog2n": round(gflops(n, batch, wall / args.steps), 1)},
+        "roofline": roofline,
+    }
+    plan.close()
+    del x, out
+    torch.cuda.empty_cache()
+
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle)")
+        result["cpu_baseline"] = cpu_baseline(x_host, n)
+    del x_host
+
+    if not args.no_breakdown:
+        flush = Flusher(torch)
+        bd = {}
+        for name in ("fft_n1024_b64_fp32", "fft_n4096_b32768_fp32", "fft_n8192_b16384_fp32",
+                     "fft_n16384_b8192_fp32", "fft_n16384_b16384_fp16"):
+            log(f"breakdown {name}")
+            bd[name] = fft_breakdown(torch, api, flush, name, args.samples)
+        for inter in (0, 1):
+            log(f"breakdown sar inter={inter}")
+            bd[f"sar_4096x4096_{'fp32' if inter == 0 else 'fp16'}_inter"] = sar_breakdown(
+                torch, api, flush, inter, args.samples)
+        result["breakdown"] = bd
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,166 @@
+/*
+ * mi355fft.h -- C ABI of the MI355X (gfx950) batched FFT and SAR library.
+ *
+ * The operations follow "Bandwidth, Not FLOPS: FFT Kernels, Matrix Units and
+ * SAR Imaging on Apple M6" (arXiv 2609.32237):
+ *   - batched complex-to-complex 1-D FFTs, each transform read once from and
+ *     written once to device memory (Section IV, eq. (1); Section VI), with
+ *     FP32 or FP16 storage and FP32 arithmetic (Section VII);
+ *   - the range-Doppler SAR image of a pulses x range-samples echo: range
+ *     compression (FFT, matched filter, inverse FFT, 1/N_r) fused in one pass,
+ *     then the azimuth FFT read straight from the columns with its 1/N_a
+ *     scale, the azimuth matched filter and the azimuth inverse FFT fused in a
+ *     second pass (Section X).
+ *
+ * Conventions shared by every entry point
+ *   - Complex values are interleaved (re, im): FP32 storage is two floats
+ *     (8 bytes) per value, FP16 storage two IEEE binary16 halves (4 bytes).
+ *   - Sizes, strides and distances count complex elements, not bytes.
+ *   - Every pointer argument named in/out/raw/ref/workspace is a DEVICE
+ *     pointer on the current HIP device; the caller owns it.
+ *   - Every call is stream-ordered on the given hipStream_t (0 = the null
+ *     stream) and never synchronises.  Argument errors are returned before
+ *     any HIP call is made.  A failed launch returns FFT_EHIP.  Faults inside
+ *     a kernel surface at the caller's next synchronisation.
+ *   - Transforms are unnormalised in both directions: forward computes
+ *     X[k] = sum_n x[n] exp(-2 pi i n k / N), inverse uses exp(+2 pi i n k / N).
+ *     Output is in natural order.
+ */
+#ifndef MI355FFT_H
+#define MI355FFT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Storage formats (Section VII: FP16 storage halves the bytes per point while
+ * the arithmetic stays FP32). */
+enum { FFT_STORAGE_FP32 = 0, FFT_STORAGE_FP16 = 1 };
+
+/* Direction = sign of the exponent. */
+enum { FFT_FORWARD = -1, FFT_INVERSE = +1 };
+
+/* Return codes. */
+enum {
+    FFT_OK = 0,
+    FFT_EINVAL = -1,       /* invalid argument (NULL, bad enum, overlapping layout) */
+    FFT_EUNSUPPORTED = -2, /* valid request this library does not implement (size) */
+    FFT_ENOMEM = -3,       /* device or host allocation failed */
+    FFT_EALIGN = -4,       /* a pointer is not aligned to one complex element */
+    FFT_EHIP = -5          /* the HIP runtime reported an error */
+};
+
+typedef struct fft_plan fft_plan; /* opaque; immutable once created */
+
+/*
+ * fft_plan_create -- plan a batch of `batch` transforms of `n` points.
+ *
+ * Section III states the problem as B transforms of N points in FP32 (the
+ * batch's footprint is its input plus its output); Section VII adds FP16
+ * storage.
+ *
+ *   n        transform length: a power of two in [1024, 16384], else
+ *            FFT_EUNSUPPORTED.
+ *   batch    number of transforms, >= 1.
+ *   stride   distance between consecutive points of one transform, >= 1.
+ *   dist     distance between the first points of consecutive transforms, >= 1.
+ *            Point j of transform b is at element b*dist + j*stride of both
+ *            the input and the output buffer.
+ *            The transforms must not overlap: either they sit in disjoint
+ *            blocks (dist >= (n-1)*stride + 1) or they interleave
+ *            (stride >= (batch-1)*dist + 1), else FFT_EINVAL.
+ *            stride == 1 selects the contiguous-row kernels; stride > 1 the
+ *            strided-column kernels (columns of a row-major matrix are
+ *            stride = row length, dist = 1).
+ *   storage  FFT_STORAGE_FP32 or FFT_STORAGE_FP16 (input and output alike).
+ *   dir      FFT_FORWARD or FFT_INVERSE.
+ *   plan_out receives the plan; untouched on error.
+ *
+ * Creates (once per device and size, shared by all plans, kept until the
+ * process ends) a device table of the n twiddle factors exp(-2 pi i m / n),
+ * computed in double precision on the host and rounded once to FP32.  Uses
+ * the current HIP device; the plan must be executed on that device.
+ * Returns FFT_OK, FFT_EINVAL, FFT_EUNSUPPORTED, FFT_ENOMEM or FFT_EHIP.
+ */
+int fft_plan_create(int64_t n, int64_t batch, int64_t stride, int64_t dist, int storage, int dir,
+                    fft_plan **plan_out);
+
+/*
+ * fft_execute -- run the planned transforms: out = FFT(in).
+ *
+ * Every transform is read from `in` once and written to `out` once (Section
+ * VI: the whole transform stays on chip between its stages).
+ *   in, out  device buffers laid out as the plan says; in == out (in place) is
+ *            allowed, partial overlap is not.  Aligned to one complex element
+ *            (8 bytes FP32, 4 bytes FP16), else FFT_EALIGN.
+ *   stream   HIP stream the kernel is launched on.
+ * Safe to call concurrently on different streams with the same plan.
+ * Returns FFT_OK, FFT_EINVAL (NULL plan or buffer), FFT_EALIGN or FFT_EHIP.
+ */
+int fft_execute(const fft_plan *plan, const void *in, void *out, hipStream_t stream);
+
+/* fft_plan_destroy -- release a plan (host memory only).  NULL is a no-op.
+ * The caller must not destroy a plan while a call using it is being made. */
+int fft_plan_destroy(fft_plan *plan);
+
+/*
+ * sar_workspace_bytes -- device workspace sar_form_image_ex needs.
+ * Holds both reference spectra and the range-compressed intermediate image
+ * (n_az * n_rg * 8 bytes for FP32, * 4 bytes for FP16 intermediates).
+ * Returns 0 for an invalid or unsupported request.
+ */
+size_t sar_workspace_bytes(int64_t n_az, int64_t n_rg, int inter_storage);
+
+/*
+ * sar_form_image_ex -- range-Doppler image of an n_az x n_rg echo (Section X).
+ *
+ *   n_az, n_rg      pulses (rows) and range samples (columns); each a power of
+ *                   two in [1024, 16384], else FFT_EUNSUPPORTED.
+ *   inter_storage   FFT_STORAGE_FP32 or FFT_STORAGE_FP16 for the one stored
+ *                   intermediate (Section X: FP16 intermediates with the
+ *                   fixed-shift scaling 1/N_r in range compression and 1/N_a on
+ *                   the azimuth FFT output).
+ *   raw             n_az x n_rg complex FP32, row-major, rows = pulses.
+ *   range_ref       n_rg complex FP32: the time-domain range reference (the
+ *                   transmitted chirp, centred and wrapped to index t mod n_rg).
+ *   az_ref          n_az complex FP32: the time-domain azimuth reference.
+ *   out             n_az x n_rg complex FP32 focused image; must not overlap
+ *                   raw or the workspace.
+ *   workspace       sar_workspace_bytes(n_az, n_rg, inter_storage) bytes,
+ *                   256-byte aligned; contents on entry are ignored.
+ *   stream          HIP stream; three kernels are launched on it in order.
+ *
+ * Computes, with H_r = FFT(range_ref) and H_a = FFT(az_ref):
+ *   y[a, :]   = IFFT( FFT(raw[a, :]) * conj(H_r) ) / n_rg      (pass 1, rows)
+ *   out[:, r] = IFFT( FFT(y[:, r]) / n_az * conj(H_a) )        (pass 2, columns)
+ * i.e. the 2-D circular cross-correlation of raw with az_ref x range_ref.
+ * Returns FFT_OK, FFT_EINVAL, FFT_EUNSUPPORTED, FFT_EALIGN, FFT_ENOMEM or
+ * FFT_EHIP.
+ */
+int sar_form_image_ex(int64_t n_az, int64_t n_rg, int inter_storage, const void *raw,
+                      const void *range_ref, const void *az_ref, void *out, void *workspace,
+                      hipStream_t stream);
+
+/*
+ * sar_form_image -- the 4096 x 4096 image with FP32 intermediates (Section X
+ * scene size).  Same as sar_form_image_ex(4096, 4096, FFT_STORAGE_FP32, ...)
+ * with a workspace the library allocates on the first call on each device and
+ * keeps until the process ends.  Calls that overlap on one device (from
+ * several threads or streams) share that workspace and race.
+ */
+int sar_form_image(const void *raw, const void *range_ref, const void *az_ref, void *out,
+                   hipStream_t stream);
+
+/* fft_strerror -- static description of a return code (never NULL). */
+const char *fft_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MI355FFT_H */

@@ -1,0 +1,148 @@
+// fft_configs.hpp -- per-size kernel shapes and the instantiation dispatcher.
+//
+// Shapes (points per thread P, transforms per workgroup C, radix sequence,
+// exchange mode, twiddle mode, persistence) are chosen for gfx950: wave64,
+// 160 KiB LDS per CU, 512 VGPRs per SIMD lane.  Rows keep one transform per
+// 256-512 threads; columns keep a strip of C adjacent columns so each row
+// access is a C-element segment.  The paper's M6 schedules (Section VI:
+// 16-8-8-8 for 8192 and 16-16-8-8 for 16384, 16 values per thread) were
+// shaped by a 32 KiB threadgroup buffer; these use larger radices because the
+// LDS is five times larger.
+//
+// Each size lists its variants; index 0 of each list is the default.  Every
+// variant computes the same transform, and the tests force each of them.
+#pragma once
+
+#include "fft_kernel.hpp"
+
+namespace mi355fft {
+
+template <int N>
+struct Configs;
+
+// Each list's defaults are given per storage (FP32, FP16): FP16 storage moves
+// half the bytes per point, so its kernels are limited by arithmetic issue and
+// prefer the higher-occupancy split exchange.  The TWMODE 0 variants are kept
+// as regression cases for the table-read twiddle path.
+//                 N     P  C  COLS   XCHG        TW PERSIST radices
+template <>
+struct Configs<1024> {
+    using Rows = KList<KCfg<1024, 16, 4, false, XCHG_SPLIT, 1, false, Radices<16, 16, 4>>,
+                       KCfg<1024, 16, 4, false, XCHG_FULL, 1, false, Radices<16, 16, 4>>,
+                       KCfg<1024, 16, 4, false, XCHG_FULL, 1, true, Radices<16, 16, 4>>,
+                       KCfg<1024, 16, 4, false, XCHG_FULL, 0, false, Radices<16, 16, 4>>>;
+    using Cols = KList<KCfg<1024, 16, 8, true, XCHG_SPLIT, 1, false, Radices<16, 16, 4>>,
+                       KCfg<1024, 16, 8, true, XCHG_FULL, 0, false, Radices<16, 16, 4>>>;
+    static constexpr int kRowDefault[2] = {1, 0}, kColDefault[2] = {0, 0};
+};
+template <>
+struct Configs<2048> {
+    using Rows = KList<KCfg<2048, 16, 2, false, XCHG_SPLIT, 1, false, Radices<16, 16, 8>>,
+                       KCfg<2048, 16, 2, false, XCHG_FULL, 1, false, Radices<16, 16, 8>>,
+                       KCfg<2048, 16, 2, false, XCHG_FULL, 1, true, Radices<16, 16, 8>>,
+                       KCfg<2048, 16, 2, false, XCHG_FULL, 0, false, Radices<16, 16, 8>>>;
+    using Cols = KList<KCfg<2048, 16, 4, true, XCHG_SPLIT, 1, false, Radices<16, 16, 8>>,
+                       KCfg<2048, 16, 4, true, XCHG_FULL, 0, false, Radices<16, 16, 8>>>;
+    static constexpr int kRowDefault[2] = {0, 0}, kColDefault[2] = {0, 0};
+};
+template <>
+struct Configs<4096> {
+    using Rows = KList<KCfg<4096, 16, 1, false, XCHG_FULL, 1, false, Radices<16, 16, 16>>,
+                       KCfg<4096, 16, 1, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>,
+                       KCfg<4096, 16, 1, false, XCHG_FULL, 1, true, Radices<16, 16, 16>>,
+                       KCfg<4096, 16, 1, false, XCHG_SPLIT, 1, true, Radices<16, 16, 16>>,
+                       KCfg<4096, 16, 1, false, XCHG_FULL, 0, false, Radices<16, 16, 16>>,
+                       KCfg<4096, 16, 1, false, XCHG_SPLIT, 0, false, Radices<16, 16, 16>>>;
+    using Cols = KList<KCfg<4096, 32, 4, true, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>,
+                       KCfg<4096, 32, 4, true, XCHG_SPLIT, 0, false, Radices<16, 16, 16>>,
+                       KCfg<4096, 16, 4, true, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>,
+                       KCfg<4096, 32, 8, true, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>>;
+    static constexpr int kRowDefault[2] = {0, 1}, kColDefault[2] = {0, 0};
+};
+template <>
+struct Configs<8192> {
+    using Rows = KList<KCfg<8192, 16, 1, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 2>>,
+                       KCfg<8192, 32, 1, false, XCHG_FULL, 1, false, Radices<32, 16, 16>>,
+                       KCfg<8192, 16, 1, false, XCHG_SPLIT, 1, true, Radices<16, 16, 16, 2>>,
+                       KCfg<8192, 16, 1, false, XCHG_FULL, 0, false, Radices<16, 16, 16, 2>>>;
+    using Cols = KList<KCfg<8192, 32, 2, true, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 2>>,
+                       KCfg<8192, 32, 2, true, XCHG_SPLIT, 0, false, Radices<16, 16, 16, 2>>>;
+    static constexpr int kRowDefault[2] = {0, 0}, kColDefault[2] = {0, 0};
+};
+template <>
+struct Configs<16384> {
+    using Rows = KList<KCfg<16384, 16, 1, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 4>>,
+                       KCfg<16384, 32, 1, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 4>>,
+                       KCfg<16384, 32, 1, false, XCHG_SPLIT, 1, true, Radices<16, 16, 16, 4>>,
+                       KCfg<16384, 32, 1, false, XCHG_SPLIT, 0, false, Radices<16, 16, 16, 4>>>;
+    using Cols = KList<KCfg<16384, 32, 1, true, XCHG_SPLIT, 0, false, Radices<16, 16, 16, 4>>,
+                       KCfg<16384, 32, 1, true, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 4>>>;
+    static constexpr int kRowDefault[2] = {1, 0}, kColDefault[2] = {1, 1};
+};
+
+template <class L>
+struct KListSize;
+template <class... Ks>
+struct KListSize<KList<Ks...>> {
+    static constexpr int value = sizeof...(Ks);
+};
+
+// Calls f(K{}) for the idx-th entry of the list.
+template <class F, class K, class... Ks>
+hipError_t with_variant(int idx, KList<K, Ks...>, F &&f) {
+    if (idx == 0) return f(K{});
+    if constexpr (sizeof...(Ks) > 0) {
+        return with_variant(idx - 1, KList<Ks...>{}, f);
+    } else {
+        return hipErrorInvalidValue;
+    }
+}
+
+// Supported (layout, storage, direction, epilogue) combinations:
+//   plain FFT:  rows or columns, input storage == output storage, either direction;
+//   matched:    forward, multiply by conj(spec) * scale, inverse:
+//               rows read FP32 and write FP32 or FP16 (range compression);
+//               columns read FP32 or FP16 and write FP32 (azimuth compression).
+template <class K>
+hipError_t dispatch_cfg(int in_st, int out_st, int inv, int epi, const void *in, void *out, const float2 *tw,
+                        const float2 *spec, const KArgs &a, hipStream_t s) {
+    if (epi == EPI_NONE) {
+        if (in_st != out_st) return hipErrorInvalidValue;
+        if (in_st == 0)
+            return inv ? launch_one<K, 0, 0, true, EPI_NONE>(in, out, tw, spec, a, s)
+                       : launch_one<K, 0, 0, false, EPI_NONE>(in, out, tw, spec, a, s);
+        return inv ? launch_one<K, 1, 1, true, EPI_NONE>(in, out, tw, spec, a, s)
+                   : launch_one<K, 1, 1, false, EPI_NONE>(in, out, tw, spec, a, s);
+    }
+    if (epi != EPI_MATCHED || inv) return hipErrorInvalidValue;
+    if constexpr (!K::COLS) {
+        if (in_st != 0) return hipErrorInvalidValue;
+        return out_st == 0 ? launch_one<K, 0, 0, false, EPI_MATCHED>(in, out, tw, spec, a, s)
+                           : launch_one<K, 0, 1, false, EPI_MATCHED>(in, out, tw, spec, a, s);
+    } else {
+        if (out_st != 0) return hipErrorInvalidValue;
+        return in_st == 0 ? launch_one<K, 0, 0, false, EPI_MATCHED>(in, out, tw, spec, a, s)
+                          : launch_one<K, 1, 0, false, EPI_MATCHED>(in, out, tw, spec, a, s);
+    }
+}
+
+template <int N>
+hipError_t dispatch(int variant, int layout, int in_st, int out_st, int inv, int epi, const void *in, void *out,
+                    const float2 *tw, const float2 *spec, const KArgs &a, hipStream_t s) {
+    auto f = [&](auto k) { return dispatch_cfg<decltype(k)>(in_st, out_st, inv, epi, in, out, tw, spec, a, s); };
+    const int half = (in_st | out_st) != 0;  // any FP16 storage involved
+    if (layout == LAYOUT_ROWS) {
+        const int v = variant < 0 ? Configs<N>::kRowDefault[half] : variant;
+        return with_variant(v, typename Configs<N>::Rows{}, f);
+    }
+    const int v = variant < 0 ? Configs<N>::kColDefault[half] : variant;
+    return with_variant(v, typename Configs<N>::Cols{}, f);
+}
+
+template <int N>
+int variant_count(int layout) {
+    return layout == LAYOUT_ROWS ? KListSize<typename Configs<N>::Rows>::value
+                                 : KListSize<typename Configs<N>::Cols>::value;
+}
+
+}  // namespace mi355fft

@@ -1,0 +1,13 @@
+// fft_n16384.hip -- instantiations of the single-pass kernels for N = 16384.
+#include "fft_configs.hpp"
+
+namespace mi355fft {
+
+hipError_t launch_fft_n16384(int variant, int layout, int in_st, int out_st, int inv, int epi, const void *in,
+                          void *out, const float2 *tw, const float2 *spec, const KArgs &a, hipStream_t s) {
+    return dispatch<16384>(variant, layout, in_st, out_st, inv, epi, in, out, tw, spec, a, s);
+}
+
+int variants_n16384(int layout) { return variant_count<16384>(layout); }
+
+}  // namespace mi355fft

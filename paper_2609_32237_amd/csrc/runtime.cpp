@@ -1,0 +1,295 @@
+// runtime.cpp -- host side of the C ABI declared in include/mi355fft.h.
+//
+// Plans validate the layout, pick the row or column kernel family, and share
+// one device twiddle table per (device, N).  Execution is one stream-ordered
+// kernel launch per call; nothing here synchronises.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstdlib>
+#include <map>
+#include <mutex>
+#include <new>
+#include <utility>
+#include <vector>
+
+#include "fft_launch.h"
+#include "mi355fft.h"
+
+using mi355fft::KArgs;
+
+struct fft_plan {
+    int64_t n, batch, stride, dist;
+    int storage, dir, device, layout, xcd_remap, variant;
+    const float2 *tw;
+};
+
+namespace {
+
+constexpr int64_t kMinN = 1024, kMaxN = 16384;
+constexpr int64_t kMaxIndex = int64_t(1) << 40;  // largest element index accepted
+
+bool is_pow2(int64_t n) { return n > 0 && (n & (n - 1)) == 0; }
+bool supported_n(int64_t n) { return is_pow2(n) && n >= kMinN && n <= kMaxN; }
+
+bool fail_alloc_hook() {
+    const char *e = std::getenv("MI355FFT_TEST_FAIL_ALLOC");
+    return e && e[0] == '1';
+}
+
+int map_hip(hipError_t e) {
+    if (e == hipSuccess) return FFT_OK;
+    if (e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation) return FFT_ENOMEM;
+    return FFT_EHIP;
+}
+
+// Twiddle tables: exp(-2 pi i m / n), m in [0, n), computed in double with the
+// angle 2 pi (m / n) (m / n is exact), rounded once to FP32.
+std::mutex g_tw_mutex;
+std::map<std::pair<int, int64_t>, float2 *> g_tw;
+
+int get_twiddles(int device, int64_t n, const float2 **out) {
+    std::lock_guard<std::mutex> lock(g_tw_mutex);
+    auto it = g_tw.find({device, n});
+    if (it != g_tw.end()) {
+        *out = it->second;
+        return FFT_OK;
+    }
+    if (fail_alloc_hook()) return FFT_ENOMEM;
+    std::vector<float2> host((size_t)n);
+    const double two_pi = 6.283185307179586476925286766559;
+    for (int64_t m = 0; m < n; ++m) {
+        const double ang = two_pi * ((double)m / (double)n);
+        host[(size_t)m] = make_float2((float)std::cos(ang), (float)-std::sin(ang));
+    }
+    float2 *dev = nullptr;
+    hipError_t e = hipMalloc((void **)&dev, sizeof(float2) * (size_t)n);
+    if (e != hipSuccess) return map_hip(e);
+    e = hipMemcpy(dev, host.data(), sizeof(float2) * (size_t)n, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        (void)hipFree(dev);
+        return map_hip(e);
+    }
+    g_tw[{device, n}] = dev;
+    *out = dev;
+    return FFT_OK;
+}
+
+hipError_t launch_fft(int64_t n, int variant, int layout, int in_st, int out_st, int inv, int epi, const void *in,
+                      void *out, const float2 *tw, const float2 *spec, const KArgs &a, hipStream_t s) {
+    using namespace mi355fft;
+    switch (n) {
+        case 1024: return launch_fft_n1024(variant, layout, in_st, out_st, inv, epi, in, out, tw, spec, a, s);
+        case 2048: return launch_fft_n2048(variant, layout, in_st, out_st, inv, epi, in, out, tw, spec, a, s);
+        case 4096: return launch_fft_n4096(variant, layout, in_st, out_st, inv, epi, in, out, tw, spec, a, s);
+        case 8192: return launch_fft_n8192(variant, layout, in_st, out_st, inv, epi, in, out, tw, spec, a, s);
+        case 16384: return launch_fft_n16384(variant, layout, in_st, out_st, inv, epi, in, out, tw, spec, a, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+int variant_count(int64_t n, int layout) {
+    using namespace mi355fft;
+    switch (n) {
+        case 1024: return variants_n1024(layout);
+        case 2048: return variants_n2048(layout);
+        case 4096: return variants_n4096(layout);
+        case 8192: return variants_n8192(layout);
+        case 16384: return variants_n16384(layout);
+        default: return 0;
+    }
+}
+
+// Kernel-shape override for tests and tuning: MI355FFT_ROW_VARIANT /
+// MI355FFT_COL_VARIANT = index into the size's variant list (unset: default).
+// Returns -1 for the default, -2 for an index the size does not have.
+int chosen_variant(int64_t n, int layout) {
+    const char *e = std::getenv(layout == mi355fft::LAYOUT_ROWS ? "MI355FFT_ROW_VARIANT" : "MI355FFT_COL_VARIANT");
+    if (!e || !e[0]) return -1;
+    char *end = nullptr;
+    long v = std::strtol(e, &end, 10);
+    if (*end != '\0' || v < 0 || v >= variant_count(n, layout)) return -2;
+    return (int)v;
+}
+
+bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// The library-owned workspace of the fixed-size sar_form_image, per device.
+std::mutex g_ws_mutex;
+std::map<int, void *> g_ws;
+
+}  // namespace
+
+extern "C" {
+
+int fft_plan_create(int64_t n, int64_t batch, int64_t stride, int64_t dist, int storage, int dir,
+                    fft_plan **plan_out) {
+    if (!plan_out) return FFT_EINVAL;
+    if (storage != FFT_STORAGE_FP32 && storage != FFT_STORAGE_FP16) return FFT_EINVAL;
+    if (dir != FFT_FORWARD && dir != FFT_INVERSE) return FFT_EINVAL;
+    if (n < 1 || batch < 1 || stride < 1 || dist < 1) return FFT_EINVAL;
+    if (!supported_n(n)) return FFT_EUNSUPPORTED;
+    // extent of the layout must be addressable
+    if (batch - 1 > kMaxIndex / dist || n - 1 > kMaxIndex / stride ||
+        (batch - 1) * dist > kMaxIndex - (n - 1) * stride)
+        return FFT_EINVAL;
+    // transforms must not overlap: disjoint blocks or interleaved
+    const bool blocks = batch == 1 || dist >= (n - 1) * stride + 1;
+    const bool interleaved = stride >= (batch - 1) * dist + 1;
+    if (!blocks && !interleaved) return FFT_EINVAL;
+    if (batch > (int64_t)0x7fffffff) return FFT_EUNSUPPORTED;  // grid size limit
+    const int layout = stride == 1 ? mi355fft::LAYOUT_ROWS : mi355fft::LAYOUT_COLS;
+    const int variant = chosen_variant(n, layout);
+    if (variant == -2) return FFT_EINVAL;
+    if (fail_alloc_hook()) return FFT_ENOMEM;  // test hook: device allocation fails
+
+    int device = 0;
+    hipError_t e = hipGetDevice(&device);
+    if (e != hipSuccess) return map_hip(e);
+    const float2 *tw = nullptr;
+    int rc = get_twiddles(device, n, &tw);
+    if (rc != FFT_OK) return rc;
+    fft_plan *p = new (std::nothrow) fft_plan;
+    if (!p) return FFT_ENOMEM;
+    p->n = n;
+    p->batch = batch;
+    p->stride = stride;
+    p->dist = dist;
+    p->storage = storage;
+    p->dir = dir;
+    p->device = device;
+    p->layout = layout;
+    p->variant = variant;
+    p->xcd_remap = layout == mi355fft::LAYOUT_COLS && dist == 1;
+    p->tw = tw;
+    *plan_out = p;
+    return FFT_OK;
+}
+
+int fft_execute(const fft_plan *plan, const void *in, void *out, hipStream_t stream) {
+    if (!plan || !in || !out) return FFT_EINVAL;
+    const size_t el = plan->storage == FFT_STORAGE_FP32 ? 8 : 4;
+    if (!aligned(in, el) || !aligned(out, el)) return FFT_EALIGN;
+    const KArgs a{plan->batch, plan->stride, plan->dist, plan->dist, 1.0f, plan->xcd_remap};
+    const int inv = plan->dir == FFT_INVERSE;
+    return map_hip(launch_fft(plan->n, plan->variant, plan->layout, plan->storage, plan->storage, inv,
+                              mi355fft::EPI_NONE, in, out, plan->tw, nullptr, a, stream));
+}
+
+int fft_plan_destroy(fft_plan *plan) {
+    delete plan;
+    return FFT_OK;
+}
+
+size_t sar_workspace_bytes(int64_t n_az, int64_t n_rg, int inter_storage) {
+    if (!supported_n(n_az) || !supported_n(n_rg)) return 0;
+    if (inter_storage != FFT_STORAGE_FP32 && inter_storage != FFT_STORAGE_FP16) return 0;
+    const size_t spectra = (size_t)(n_az + n_rg) * sizeof(float2);  // multiple of 256 bytes
+    const size_t el = inter_storage == FFT_STORAGE_FP32 ? 8 : 4;
+    return spectra + (size_t)n_az * (size_t)n_rg * el;
+}
+
+int sar_form_image_ex(int64_t n_az, int64_t n_rg, int inter_storage, const void *raw, const void *range_ref,
+                      const void *az_ref, void *out, void *workspace, hipStream_t stream) {
+    if (!raw || !range_ref || !az_ref || !out || !workspace) return FFT_EINVAL;
+    if (inter_storage != FFT_STORAGE_FP32 && inter_storage != FFT_STORAGE_FP16) return FFT_EINVAL;
+    if (n_az < 1 || n_rg < 1) return FFT_EINVAL;
+    if (!supported_n(n_az) || !supported_n(n_rg)) return FFT_EUNSUPPORTED;
+    if (!aligned(raw, 8) || !aligned(range_ref, 8) || !aligned(az_ref, 8) || !aligned(out, 8) ||
+        !aligned(workspace, 256))
+        return FFT_EALIGN;
+    const size_t img = (size_t)n_az * (size_t)n_rg * 8;
+    const size_t ws = sar_workspace_bytes(n_az, n_rg, inter_storage);
+    auto overlap = [](const void *a, size_t na, const void *b, size_t nb) {
+        const char *pa = (const char *)a, *pb = (const char *)b;
+        return pa < pb + nb && pb < pa + na;
+    };
+    if (overlap(out, img, raw, img) || overlap(out, img, workspace, ws) || overlap(raw, img, workspace, ws))
+        return FFT_EINVAL;
+
+    int device = 0;
+    hipError_t e = hipGetDevice(&device);
+    if (e != hipSuccess) return map_hip(e);
+    const float2 *tw_rg = nullptr, *tw_az = nullptr;
+    int rc = get_twiddles(device, n_rg, &tw_rg);
+    if (rc == FFT_OK) rc = get_twiddles(device, n_az, &tw_az);
+    if (rc != FFT_OK) return rc;
+
+    const int vrow = chosen_variant(n_rg, mi355fft::LAYOUT_ROWS);
+    const int vcol = chosen_variant(n_az, mi355fft::LAYOUT_COLS);
+    const int vref = chosen_variant(n_az, mi355fft::LAYOUT_ROWS);
+    if (vrow == -2 || vcol == -2 || vref == -2) return FFT_EINVAL;
+
+    float2 *h_rg = reinterpret_cast<float2 *>(workspace);
+    float2 *h_az = h_rg + n_rg;
+    void *mid = h_az + n_az;
+    using mi355fft::EPI_MATCHED;
+    using mi355fft::EPI_NONE;
+    using mi355fft::LAYOUT_COLS;
+    using mi355fft::LAYOUT_ROWS;
+
+    // reference spectra H = FFT(ref) into the workspace; the passes multiply by
+    // conj(H).  Equal lengths: one launch of two transforms (the input distance
+    // is the signed distance between the two reference buffers).
+    if (n_rg == n_az) {
+        const long long gap = ((const char *)az_ref - (const char *)range_ref) / (long long)sizeof(float2);
+        const KArgs a{2, 1, gap, n_rg, 1.0f, 0};
+        e = launch_fft(n_rg, vrow, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, range_ref, h_rg, tw_rg, nullptr, a, stream);
+        if (e != hipSuccess) return map_hip(e);
+    } else {
+        const KArgs a1{1, 1, n_rg, n_rg, 1.0f, 0};
+        e = launch_fft(n_rg, vrow, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, range_ref, h_rg, tw_rg, nullptr, a1, stream);
+        if (e != hipSuccess) return map_hip(e);
+        const KArgs a2{1, 1, n_az, n_az, 1.0f, 0};
+        e = launch_fft(n_az, vref, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, az_ref, h_az, tw_az, nullptr, a2, stream);
+        if (e != hipSuccess) return map_hip(e);
+    }
+
+    // pass 1, rows (range): FFT, * conj(H_r) / n_rg, IFFT -> intermediate
+    const KArgs ar{n_az, 1, n_rg, n_rg, (float)(1.0 / (double)n_rg), 0};
+    e = launch_fft(n_rg, vrow, LAYOUT_ROWS, FFT_STORAGE_FP32, inter_storage, 0, EPI_MATCHED, raw, mid, tw_rg, h_rg,
+                   ar, stream);
+    if (e != hipSuccess) return map_hip(e);
+
+    // pass 2, columns (azimuth): FFT, / n_az * conj(H_a), IFFT -> image
+    const KArgs ac{n_rg, n_rg, 1, 1, (float)(1.0 / (double)n_az), 1};
+    e = launch_fft(n_az, vcol, LAYOUT_COLS, inter_storage, FFT_STORAGE_FP32, 0, EPI_MATCHED, mid, out, tw_az, h_az,
+                   ac, stream);
+    return map_hip(e);
+}
+
+int sar_form_image(const void *raw, const void *range_ref, const void *az_ref, void *out, hipStream_t stream) {
+    if (!raw || !range_ref || !az_ref || !out) return FFT_EINVAL;
+    if (fail_alloc_hook()) return FFT_ENOMEM;  // test hook: device allocation fails
+    int device = 0;
+    hipError_t e = hipGetDevice(&device);
+    if (e != hipSuccess) return map_hip(e);
+    void *ws = nullptr;
+    {
+        std::lock_guard<std::mutex> lock(g_ws_mutex);
+        auto it = g_ws.find(device);
+        if (it != g_ws.end()) {
+            ws = it->second;
+        } else {
+            e = hipMalloc(&ws, sar_workspace_bytes(4096, 4096, FFT_STORAGE_FP32));
+            if (e != hipSuccess) return map_hip(e);
+            g_ws[device] = ws;
+        }
+    }
+    return sar_form_image_ex(4096, 4096, FFT_STORAGE_FP32, raw, range_ref, az_ref, out, ws, stream);
+}
+
+const char *fft_strerror(int code) {
+    switch (code) {
+        case FFT_OK: return "success";
+        case FFT_EINVAL: return "invalid argument";
+        case FFT_EUNSUPPORTED: return "unsupported size or configuration";
+        case FFT_ENOMEM: return "out of memory";
+        case FFT_EALIGN: return "pointer not aligned to one complex element";
+        case FFT_EHIP: return "HIP runtime error";
+        default: return "unknown error code";
+    }
+}
+
+}  // extern "C"

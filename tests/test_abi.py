@@ -1,0 +1,147 @@
+"""Host-side checks of the C ABI: symbols, argument errors, error strings.
+
+None of these make a compute call, so they run without a GPU: every argument
+error is returned before the library touches the HIP runtime.
+"""
+import ctypes
+import os
+import re
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mi355fft.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2609_32237_amd import _lib
+
+    return _lib
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b([a-z_][a-z0-9_]*)\s*\([^;{]*\)\s*;", text)))
+
+
+def test_header_declares_the_abi():
+    assert declared_functions() == sorted(
+        ["fft_plan_create", "fft_execute", "fft_plan_destroy", "sar_workspace_bytes", "sar_form_image_ex",
+         "sar_form_image", "fft_strerror"])
+
+
+def test_library_exports_every_declared_symbol(L):
+    out = subprocess.run(["nm", "-D", "--defined-only", L.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(re.findall(r" T (\w+)$", out, flags=re.M))
+    for name in declared_functions():
+        assert name in exported, name
+        assert hasattr(L.lib, name)
+    assert set(L.EXPORTS) == set(declared_functions())
+
+
+def test_header_compiles_as_c():
+    """The header is plain C: it compiles with gcc against the HIP runtime headers."""
+    src = f'#include "{HEADER}"\nint main(void) {{ return FFT_OK; }}\n'
+    res = subprocess.run(["gcc", "-x", "c", "-std=c11", "-fsyntax-only", "-D__HIP_PLATFORM_AMD__",
+                          "-I/opt/rocm/include", "-"], input=src, capture_output=True, text=True)
+    assert res.returncode == 0, res.stderr
+
+
+def test_strerror_covers_every_code(L):
+    codes = [L.FFT_OK, L.FFT_EINVAL, L.FFT_EUNSUPPORTED, L.FFT_ENOMEM, L.FFT_EALIGN, L.FFT_EHIP]
+    msgs = [L.fft_strerror(c) for c in codes]
+    assert len(set(msgs)) == len(codes)
+    assert "unknown" not in " ".join(msgs)
+    assert L.fft_strerror(12345) == "unknown error code"
+
+
+def create(L, *args):
+    p = ctypes.c_void_p()
+    return L.lib.fft_plan_create(*args, ctypes.byref(p)), p
+
+
+@pytest.mark.parametrize("args, code", [
+    ((1000, 1, 1, 1000, 0, -1), "FFT_EUNSUPPORTED"),   # not a power of two
+    ((512, 1, 1, 512, 0, -1), "FFT_EUNSUPPORTED"),     # below 1024
+    ((32768, 1, 1, 32768, 0, -1), "FFT_EUNSUPPORTED"), # above 16384
+    ((0, 1, 1, 1, 0, -1), "FFT_EINVAL"),
+    ((4096, 0, 1, 4096, 0, -1), "FFT_EINVAL"),         # empty batch
+    ((4096, -3, 1, 4096, 0, -1), "FFT_EINVAL"),
+    ((4096, 2, 0, 4096, 0, -1), "FFT_EINVAL"),         # stride 0
+    ((4096, 2, 1, 0, 0, -1), "FFT_EINVAL"),            # dist 0
+    ((4096, 2, 1, 4095, 0, -1), "FFT_EINVAL"),         # rows overlap
+    ((4096, 8, 4, 1, 0, -1), "FFT_EINVAL"),            # columns overlap (stride < batch)
+    ((4096, 3, 2, 2, 0, -1), "FFT_EINVAL"),            # neither blocks nor interleaved
+    ((4096, 1, 1, 4096, 2, -1), "FFT_EINVAL"),         # bad storage
+    ((4096, 1, 1, 4096, 0, 0), "FFT_EINVAL"),          # bad direction
+    ((4096, 1 << 30, 1, 1 << 30, 0, -1), "FFT_EINVAL"),  # layout beyond 2^40 elements
+])
+def test_plan_argument_errors(L, args, code):
+    rc, p = create(L, *args)
+    assert rc == getattr(L, code)
+    assert p.value is None
+
+
+def test_plan_null_out(L):
+    assert L.lib.fft_plan_create(4096, 1, 1, 4096, 0, -1, None) == L.FFT_EINVAL
+
+
+def test_execute_and_destroy_null(L):
+    assert L.lib.fft_execute(None, 256, 256, None) == L.FFT_EINVAL
+    assert L.lib.fft_plan_destroy(None) == L.FFT_OK
+
+
+def test_sar_argument_errors(L):
+    f = L.lib.sar_form_image_ex
+    ok = 1 << 20
+    assert f(4096, 4096, 0, None, ok, ok, ok, ok, None) == L.FFT_EINVAL
+    assert f(4096, 4096, 3, ok, ok, ok, ok, ok, None) == L.FFT_EINVAL
+    assert f(4000, 4096, 0, ok, ok, ok, ok, ok, None) == L.FFT_EUNSUPPORTED
+    assert f(4096, 32768, 0, ok, ok, ok, ok, ok, None) == L.FFT_EUNSUPPORTED
+    assert f(4096, 4096, 0, ok + 4, ok, ok, 1 << 40, 1 << 41, None) == L.FFT_EALIGN
+    assert f(4096, 4096, 0, ok, ok, ok, 1 << 40, (1 << 41) + 8, None) == L.FFT_EALIGN  # workspace 256 B
+    # out overlapping raw
+    assert f(4096, 4096, 0, 1 << 30, ok, ok, (1 << 30) + 4096, 1 << 40, None) == L.FFT_EINVAL
+    assert L.lib.sar_form_image(None, ok, ok, ok, None) == L.FFT_EINVAL
+
+
+def test_sar_workspace_bytes(L):
+    assert L.sar_workspace_bytes(4096, 4096, 0) == (4096 + 4096) * 8 + 4096 * 4096 * 8
+    assert L.sar_workspace_bytes(4096, 4096, 1) == (4096 + 4096) * 8 + 4096 * 4096 * 4
+    assert L.sar_workspace_bytes(1024, 16384, 1) == (1024 + 16384) * 8 + 1024 * 16384 * 4
+    assert L.sar_workspace_bytes(4096, 4000, 0) == 0
+    assert L.sar_workspace_bytes(4096, 4096, 5) == 0
+
+
+def test_forced_allocation_failure_reports_enomem():
+    """MI355FFT_TEST_FAIL_ALLOC=1 makes the first device allocation fail."""
+    code = ("import ctypes\n"
+            "from paper_2609_32237_amd import _lib as L\n"
+            "p = ctypes.c_void_p()\n"
+            "print(L.lib.fft_plan_create(4096, 2, 1, 4096, 0, -1, ctypes.byref(p)), p.value)\n")
+    env = dict(os.environ, MI355FFT_TEST_FAIL_ALLOC="1")
+    res = subprocess.run([sys.executable, "-c", code], cwd=ROOT, env=env, capture_output=True, text=True,
+                         timeout=120)
+    assert res.returncode == 0, res.stderr
+    rc, val = res.stdout.split()
+    assert int(rc) == -3 and val == "None"
+
+
+@pytest.mark.parametrize("var, value", [("MI355FFT_ROW_VARIANT", "99"), ("MI355FFT_ROW_VARIANT", "x"),
+                                        ("MI355FFT_COL_VARIANT", "-1")])
+def test_out_of_range_variant_is_rejected_before_any_hip_call(var, value):
+    stride, dist = (1, 4096) if var == "MI355FFT_ROW_VARIANT" else (8, 1)
+    code = ("import ctypes\n"
+            "from paper_2609_32237_amd import _lib as L\n"
+            "p = ctypes.c_void_p()\n"
+            f"print(L.lib.fft_plan_create(4096, 2, {stride}, {dist}, 0, -1, ctypes.byref(p)))\n")
+    env = dict(os.environ, **{var: value})
+    res = subprocess.run([sys.executable, "-c", code], cwd=ROOT, env=env, capture_output=True, text=True,
+                         timeout=120)
+    assert res.returncode == 0, res.stderr
+    assert int(res.stdout.split()[0]) == -1

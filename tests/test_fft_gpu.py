@@ -1,0 +1,225 @@
+"""Batched FFT parity: the HIP kernels through the C ABI against the fp64 oracle.
+
+Tolerances (relative L2 per transform, maximised over the batch): 1e-5 for
+FP32 storage, 3e-3 for FP16 storage on the FP16-rounded input.  The paper's
+own kernels reach 3.6e-7 .. 8.2e-7 (FP32) and 73.6 dB SQNR, about 2.1e-4 (FP16)
+(Sections III, VI and VII), so both bounds carry over ten times margin.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from gpu_util import log, rel_rows, to_dev, to_host, widen
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"fp32": 1e-5, "fp16": 3e-3}
+SIZES = [1024, 2048, 4096, 8192, 16384]
+
+
+@pytest.fixture(scope="module")
+def api():
+    import torch
+
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2609_32237_amd import _lib, torch_api
+
+    return torch_api
+
+
+def storage_code(storage):
+    return 0 if storage == "fp32" else 1
+
+
+def run_plan(api, x_host, n, batch, stride, dist, storage, direction, inplace=False):
+    import torch
+
+    xd = to_dev(x_host)
+    # out of place, the output starts as a copy of the input so that entries the
+    # layout does not cover can be checked for being left alone
+    out = xd if inplace else xd.clone()
+    plan = api.Plan(n, batch, stride, dist, storage_code(storage), direction)
+    plan.execute(xd, out)
+    torch.cuda.synchronize()
+    plan.close()
+    return to_host(out)
+
+
+def make_input(storage, shape, seed):
+    if storage == "fp32":
+        b, n = shape
+        return workloads.uniform_complex(b, n, seed)
+    return workloads.uniform_complex(shape[0], shape[1], seed, "fp16")
+
+
+@pytest.mark.parametrize("n", SIZES)
+@pytest.mark.parametrize("storage", ["fp32", "fp16"])
+@pytest.mark.parametrize("direction", [-1, 1])
+@pytest.mark.parametrize("batch", [1, 3, 257])
+def test_rows(api, n, storage, direction, batch):
+    """Contiguous rows, ragged batches (257 is not a multiple of any workgroup's transform count)."""
+    log(f"rows n={n} {storage} dir={direction} batch={batch}")
+    x = make_input(storage, (batch, n), 100 + n + batch)
+    y = widen(run_plan(api, x, n, batch, 1, n, storage, direction))
+    ref = oracle.fft(x, direction)
+    err = rel_rows(y, ref)
+    assert err.max() < TOL[storage], err.max()
+
+
+@pytest.mark.parametrize("n", SIZES)
+@pytest.mark.parametrize("storage", ["fp32", "fp16"])
+@pytest.mark.parametrize("direction", [-1, 1])
+@pytest.mark.parametrize("cols, width", [(1, 1), (5, 5), (37, 40)])
+def test_columns(api, n, storage, direction, cols, width):
+    """Columns of a row-major (n, width) matrix: stride = width, dist = 1.
+    Columns beyond ``cols`` must be left untouched."""
+    log(f"cols n={n} {storage} dir={direction} cols={cols} width={width}")
+    m = make_input(storage, (n, width), 200 + n + cols)
+    y = run_plan(api, m, n, cols, width, 1, storage, direction)
+    ref = oracle.fft_layout(m, n, cols, width, 1, direction).reshape(n, width)
+    err = rel_rows(widen(y).T[:cols], ref.T[:cols])
+    assert err.max() < TOL[storage], err.max()
+    if width > cols:
+        assert np.array_equal(y[:, cols:], m[:, cols:])
+
+
+@pytest.mark.parametrize("n", SIZES)
+@pytest.mark.parametrize("storage", ["fp32", "fp16"])
+def test_in_place(api, n, storage):
+    log(f"in-place n={n} {storage}")
+    x = make_input(storage, (9, n), 300 + n)
+    y = widen(run_plan(api, x, n, 9, 1, n, storage, -1, inplace=True))
+    assert rel_rows(y, oracle.fft(x)).max() < TOL[storage]
+
+
+@pytest.mark.parametrize("n", [1024, 4096, 16384])
+def test_padded_rows_and_strided_blocks(api, n):
+    """dist > n leaves the gaps alone; stride 3 with dist 3n uses the column kernel on blocks."""
+    log(f"padded/strided n={n}")
+    batch, dist = 5, n + 7
+    buf = workloads.uniform_complex(1, batch * dist, 400 + n)[0]
+    y = run_plan(api, buf, n, batch, 1, dist, "fp32", -1)
+    ref = oracle.fft_layout(buf, n, batch, 1, dist, -1)
+    yb, rb = y.reshape(batch, dist), ref.reshape(batch, dist)
+    assert rel_rows(yb[:, :n], rb[:, :n]).max() < 1e-5
+    assert np.array_equal(yb[:, n:], buf.reshape(batch, dist)[:, n:])
+    buf = workloads.uniform_complex(1, batch * 3 * n, 500 + n)[0]
+    y = run_plan(api, buf, n, batch, 3, 3 * n, "fp32", 1)
+    ref = oracle.fft_layout(buf, n, batch, 3, 3 * n, 1)
+    yb, rb = y.reshape(batch, n, 3), ref.reshape(batch, n, 3)
+    assert rel_rows(yb[:, :, 0], rb[:, :, 0]).max() < 1e-5
+    assert np.array_equal(yb[:, :, 1:], buf.reshape(batch, n, 3)[:, :, 1:])
+
+
+@pytest.mark.parametrize("n", SIZES)
+def test_closed_forms(api, n):
+    """Impulse -> exp(-2 pi i k n0 / N); tone -> N delta[k - f]; constant -> N delta[k]."""
+    log(f"closed forms n={n}")
+    k = np.arange(n)
+    n0, f = n // 3, n // 5
+    x = np.zeros((3, n), np.complex64)
+    x[0, n0] = 1
+    x[1] = np.exp(2j * np.pi * ((f * k) % n) / n)
+    x[2] = 1
+    y = widen(run_plan(api, x, n, 3, 1, n, "fp32", -1))
+    want = np.zeros((3, n), complex)
+    want[0] = np.exp(-2j * np.pi * ((k * n0) % n) / n)
+    want[1, f] = n
+    want[2, 0] = n
+    assert np.abs(y[0] - want[0]).max() < 1e-6
+    assert np.abs(y[1] - want[1]).max() < 1e-6 * n
+    assert np.abs(y[2] - want[2]).max() < 1e-6 * n
+
+
+def test_non_default_stream(api):
+    import torch
+
+    log("non-default stream")
+    x = workloads.uniform_complex(64, 4096, 7)
+    xd = to_dev(x)
+    out = torch.empty_like(xd)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        api.fft(xd, -1, out=out)
+    s.synchronize()
+    assert rel_rows(widen(to_host(out)), oracle.fft(x)).max() < 1e-5
+
+
+def test_misaligned_pointer(api):
+    import torch
+
+    from paper_2609_32237_amd import _lib
+
+    buf = torch.zeros(4096 * 2 + 1, dtype=torch.complex64, device="cuda")
+    plan = _lib.fft_plan_create(4096, 1, 1, 4096, 0, -1)
+    try:
+        rc = _lib.lib.fft_execute(plan, buf.data_ptr() + 4, buf.data_ptr(), None)
+        assert rc == _lib.FFT_EALIGN
+        rc = _lib.lib.fft_execute(plan, buf.data_ptr(), buf.data_ptr() + 4, None)
+        assert rc == _lib.FFT_EALIGN
+    finally:
+        _lib.fft_plan_destroy(plan)
+
+
+# --------------------------------------------------------------------------
+# The benchmark workloads at full size, in the launch configuration the
+# benchmark times: sampled transforms against the oracle, Parseval on all.
+# --------------------------------------------------------------------------
+
+FULL = ["fft_n1024_b64_fp32", "fft_n4096_b32768_fp32", "fft_n8192_b16384_fp32", "fft_n16384_b8192_fp32",
+        "fft_n16384_b16384_fp16"]
+
+
+def sample_rows(batch, k=48, seed=0):
+    rng = np.random.default_rng(seed)
+    rows = {0, 1, batch - 2, batch - 1} | set(rng.integers(0, batch, k).tolist())
+    return np.array(sorted(r for r in rows if 0 <= r < batch))
+
+
+def parseval_ratio(x, y):
+    """sum |Y|^2 / (N sum |x|^2) per transform, accumulated in fp64."""
+    x, y = widen(x), widen(y)
+    n = x.shape[-1]
+    return (np.abs(y) ** 2).sum(-1) / (n * (np.abs(x) ** 2).sum(-1))
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_full_size_workload(api, name):
+    import torch
+
+    w = workloads.FFT_WORKLOADS[name]
+    n, batch, storage = w["n"], w["batch"], w["storage"]
+    log(f"full-size {name}")
+    x = workloads.fft_workload(name)
+    xd = to_dev(x)
+    out = torch.empty_like(xd)
+    plan = api.Plan(n, batch, 1, n, storage_code(storage), -1)
+    plan.execute(xd, out)
+    torch.cuda.synchronize()
+    y = to_host(out)
+    rows = sample_rows(batch) if batch > 64 else np.arange(batch)
+    ref = oracle.fft(x[rows])
+    err = rel_rows(widen(y[rows]), ref)
+    log(f"  {name}: max rel {err.max():.3e}  SQNR {-20 * np.log10(err.max()):.1f} dB")
+    assert err.max() < TOL[storage]
+    # Parseval on every transform, in chunks
+    tol = 2e-5 if storage == "fp32" else 5e-3
+    for s in range(0, batch, 2048):
+        r = parseval_ratio(x[s:s + 2048], y[s:s + 2048])
+        assert np.abs(r - 1).max() < tol, (s, np.abs(r - 1).max())
+    if name == "fft_n4096_b32768_fp32":
+        # round trip: inverse of the forward output equals N x
+        inv = api.Plan(n, batch, 1, n, 0, 1)
+        back = torch.empty_like(xd)
+        inv.execute(out, back)
+        torch.cuda.synchronize()
+        b = to_host(back)
+        err = rel_rows(widen(b[rows]) / n, x[rows].astype(np.complex128))
+        log(f"  round trip max rel {err.max():.3e}")
+        assert err.max() < 1e-5
+        d = (b / np.float32(n) - x)
+        glob = np.sqrt((np.abs(d.astype(np.complex128)) ** 2).sum() / (np.abs(x.astype(np.complex128)) ** 2).sum())
+        assert glob < 1e-5
+        inv.close()
+    plan.close()
