@@ -123,7 +123,8 @@ def sar_breakdown(torch, api, flush, inter, samples):
 
 
 def cpu_baseline(x_host, n, target_s=10.0):
-    """The fp64 oracle on a bounded sample of the workload, on this host's cores."""
+    """The fp64 oracle on a bounded sample of the workload, on this host's cores
+    (median of three timings of the same sample)."""
     import oracle
 
     threads = oracle.default_threads()
@@ -131,14 +132,35 @@ def cpu_baseline(x_host, n, target_s=10.0):
     t0 = time.perf_counter()
     oracle.fft(x_host[:probe], nthreads=threads)
     t_probe = time.perf_counter() - t0
-    count = int(min(x_host.shape[0], max(probe, probe * target_s / max(t_probe, 1e-6))))
-    sample = x_host[:count]
-    xs = sample.astype(np.complex128)  # widening is not timed
-    t0 = time.perf_counter()
-    oracle.fft_layout(xs, n, count, 1, n, -1, nthreads=threads)
-    dt = time.perf_counter() - t0
+    count = int(min(x_host.shape[0], max(probe, probe * target_s / 3 / max(t_probe, 1e-6))))
+    xs = x_host[:count].astype(np.complex128)  # widening is not timed
+    times = []
+    for _ in range(3):
+        t0 = time.perf_counter()
+        oracle.fft_layout(xs, n, count, 1, n, -1, nthreads=threads)
+        times.append(time.perf_counter() - t0)
+    dt = float(np.median(times))
     return {"value": round(16.0 * n * count / dt / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {count} of {x_host.shape[0]} transforms (N={n}, fp64 radix-2, {dt:.1f} s)"}
+            "sample": f"first {count} of {x_host.shape[0]} transforms (N={n}, fp64 radix-2), median of 3 "
+                      f"timings, {dt:.2f} s each"}
+
+
+def copy_reference(torch):
+    """Read+write bandwidth of a plain streaming kernel on this GPU: an in-place
+    scale of a 1 GiB buffer (reads and writes every byte once), median of 10."""
+    buf = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+    for _ in range(3):
+        buf.mul_(1.0)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(10)]
+    for a, b in ev:
+        a.record()
+        buf.mul_(1.0)
+        b.record()
+    torch.cuda.synchronize()
+    ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
+    del buf
+    torch.cuda.empty_cache()
+    return 2.0 * (1 << 30) / (ms * 1e-3) / 1e9
 
 
 def load_traffic(digest: str):
@@ -151,7 +173,83 @@ def load_traffic(digest: str):
     return rec.get("bytes_per_launch")
 
 
+def summarize(prof_dir: str, command: str) -> str:
+    """Text summary of rocprofv3 CSV output: per-kernel durations (kernel trace)
+    or per-dispatch counter values (--pmc), for committing under profiles/."""
+    import csv
+    import glob
+    from collections import defaultdict
+
+    lines = [f"command: {command}", f"source: {prof_dir}"]
+    traces = glob.glob(os.path.join(prof_dir, "**", "*kernel_trace.csv"), recursive=True)
+    pmcs = glob.glob(os.path.join(prof_dir, "**", "*counter_collection.csv"), recursive=True)
+    for path in traces:
+        groups = defaultdict(list)
+        for r in csv.DictReader(open(path)):
+            key = (r["Kernel_Name"], r["Grid_Size_X"], r["Workgroup_Size_X"], r["LDS_Block_Size"],
+                   r["VGPR_Count"], r["Scratch_Size"])
+            groups[key].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+        lines.append("kernel trace (durations in us): calls, mean, median, min, max | grid, wg, lds, vgpr, scratch | name")
+        for key, d in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
+            d = np.array(d)
+            lines.append(f"{len(d):5d} {d.mean():10.2f} {np.median(d):10.2f} {d.min():10.2f} {d.max():10.2f} | "
+                         f"{key[1]} {key[2]} {key[3]} {key[4]} {key[5]} | {key[0][:200]}")
+    for path in pmcs:
+        groups = defaultdict(list)
+        for r in csv.DictReader(open(path)):
+            groups[(r["Kernel_Name"], r["Grid_Size"], r["Counter_Name"])].append(float(r["Counter_Value"]))
+        lines.append("counters per dispatch: dispatches, mean value | grid | counter | name")
+        for key, v in sorted(groups.items()):
+            lines.append(f"{len(v):5d} {np.mean(v):16.1f} | {key[1]} | {key[2]} | {key[0][:200]}")
+    return "\n".join(lines) + "\n"
+
+
+def _pmc_means(prof_dir: str, counter: str):
+    """{(kernel name, grid): mean counter value per dispatch} from a --pmc run."""
+    import csv
+    import glob
+    from collections import defaultdict
+
+    vals = defaultdict(list)
+    for path in glob.glob(os.path.join(prof_dir, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] == counter:
+                vals[(r["Kernel_Name"], int(r["Grid_Size"]))].append(float(r["Counter_Value"]))
+    return {k: float(np.mean(v)) for k, v in vals.items()}
+
+
+def make_traffic(fetch_dir: str, write_dir: str, commands: list) -> dict:
+    """HBM-side bytes per launch of the benchmarked FFT kernel from two --pmc runs
+    (FETCH_SIZE, WRITE_SIZE; KiB per dispatch), each scaled by what the same
+    counter reads for the copy-reference kernel, which reads and writes exactly
+    1 GiB per dispatch."""
+    rec = {"workload": WORKLOAD, "kernel_source_digest": kernel_source_digest(), "commands": commands}
+    n, batch = 4096, 32768
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        means = _pmc_means(d, counter)
+        fft = [v for (name, grid), v in means.items() if "fft_kernel<mi355fft::KCfg<4096," in name
+               and grid == batch * 256 and "(mi355fft::EPI" not in name]
+        calib = [v for (name, grid), v in means.items() if "MulFunctor" in name and grid >= (1 << 26)]
+        if not fft or not calib:
+            raise RuntimeError(f"{counter}: benchmark or reference kernel missing in {d}")
+        factor = ((1 << 30) / 1024.0) / calib[0]
+        key = "fetch" if counter == "FETCH_SIZE" else "write"
+        rec[f"{key}_kib_per_dispatch_raw"] = fft[0]
+        rec[f"{key}_reference_kib_per_dispatch_raw"] = calib[0]
+        rec[f"{key}_scale"] = factor
+        rec[f"{key}_bytes_per_launch"] = fft[0] * 1024.0 * factor
+    rec["algorithmic_bytes_per_launch"] = 16 * n * batch
+    rec["bytes_per_launch"] = rec["fetch_bytes_per_launch"] + rec["write_bytes_per_launch"]
+    return rec
+
+
 def main():
+    if len(sys.argv) > 1 and sys.argv[1] == "--summarize":
+        print(summarize(sys.argv[2], " ".join(sys.argv[3:])), end="")
+        return
+    if len(sys.argv) > 1 and sys.argv[1] == "--make-traffic":
+        print(json.dumps(make_traffic(sys.argv[2], sys.argv[3], sys.argv[4:]), indent=1))
+        return
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
@@ -159,8 +257,6 @@ def main():
     ap.add_argument("--samples", type=int, default=11, help="cache-flushed samples per breakdown workload")
     ap.add_argument("--no-breakdown", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--copy-calib", action="store_true",
-                    help="also run an in-place scale of a 1 GiB buffer (known traffic) for counter calibration")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on one GPU; --gpus must be 1",
@@ -182,13 +278,6 @@ def main():
     plan = api.Plan(n, batch, 1, n, 0, -1)
     step_bytes = 2 * 8 * n * batch
 
-    if args.copy_calib:
-        cal = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
-        for _ in range(3):
-            cal.mul_(1.0)
-        torch.cuda.synchronize()
-        del cal
-
     for _ in range(args.warmup):
         plan.execute(x, out)
     torch.cuda.synchronize()
@@ -208,10 +297,15 @@ def main():
     achieved = step_bytes / (kernel_ms * 1e-3) / 1e9
 
     digest = kernel_source_digest()
+    plan.close()
+    del x, out
+    torch.cuda.empty_cache()
+    copy_gbs = copy_reference(torch)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": load_traffic(digest),
                 "kernel": "fft_kernel rows N=4096 fp32 forward", "algorithmic_bytes_per_launch": step_bytes,
-                "avg_launch_ms": round(kernel_ms, 5), "kernel_source_digest": digest}
+                "avg_launch_ms": round(kernel_ms, 5), "kernel_source_digest": digest,
+                "measured_copy_GBs": round(copy_gbs, 1), "frac_of_measured_copy": round(achieved / copy_gbs, 4)}
     result = {
         "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(wall * 1e3 / args.steps, 5), "higher_is_better": True,
@@ -221,9 +315,6 @@ def main():
                    "gflops_5nlog2n": round(gflops(n, batch, wall / args.steps), 1)},
         "roofline": roofline,
     }
-    plan.close()
-    del x, out
-    torch.cuda.empty_cache()
 
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
