@@ -177,13 +177,33 @@ struct Dft {
 // caches); intermediates that the next kernel reads soon are stored normally
 // so they can stay in the 256 MiB Infinity Cache.  Loads carry no hint (the
 // hint measured slower on loads).
+//
+// Two addressing forms: raw buffer accesses (a per-workgroup resource built
+// from a uniform base, one 32-bit lane offset, and a scalar offset per
+// register: no per-access vector address arithmetic), and plain 64-bit
+// pointers for layouts whose per-workgroup span does not fit 31 bits.
+using rsrc_t = __amdgpu_buffer_rsrc_t;
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+constexpr int kBufferFlags = 0x00020000;  // raw buffer, 32-bit data format
+constexpr int kNtAux = 2;                 // cache-policy bit of the non-temporal hint
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void *base, unsigned bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, kBufferFlags);
+}
+
 template <int STORAGE>
 struct Store;
 
 template <>
 struct Store<0> {  // complex FP32, 8 bytes
     using T = float2;
+    static constexpr int BYTES = 8;
     __device__ __forceinline__ static float2 load(const T *p) { return *p; }
+    __device__ __forceinline__ static float2 load(rsrc_t r, unsigned voff, unsigned soff) {
+        return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
+    }
     template <bool NT>
     __device__ __forceinline__ static void store(T *p, float2 v) {
         if constexpr (NT) {
@@ -193,28 +213,39 @@ struct Store<0> {  // complex FP32, 8 bytes
             *p = v;
         }
     }
+    template <bool NT>
+    __device__ __forceinline__ static void store(rsrc_t r, unsigned voff, unsigned soff, float2 v) {
+        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2_t, v), r, voff, soff, NT ? kNtAux : 0);
+    }
 };
 
 template <>
 struct Store<1> {  // complex FP16 (binary16 pair), 4 bytes; FP32 arithmetic
     using T = __half2;
-    __device__ __forceinline__ static float2 load(const T *p) {
-        const unsigned int bits = *reinterpret_cast<const unsigned int *>(p);
-        const _Float16 lo = __builtin_bit_cast(_Float16, (unsigned short)(bits & 0xffffu));
-        const _Float16 hi = __builtin_bit_cast(_Float16, (unsigned short)(bits >> 16));
-        return make_float2((float)lo, (float)hi);
+    static constexpr int BYTES = 4;
+    __device__ __forceinline__ static float2 widen(unsigned int bits) {
+        const f32x2_t f = __builtin_convertvector(__builtin_bit_cast(f16x2_t, bits), f32x2_t);
+        return make_float2(f.x, f.y);
+    }
+    // round to nearest even (the conversion's default rounding mode)
+    __device__ __forceinline__ static unsigned int narrow(float2 v) {
+        return __builtin_bit_cast(unsigned int, __builtin_convertvector((f32x2_t){v.x, v.y}, f16x2_t));
+    }
+    __device__ __forceinline__ static float2 load(const T *p) { return widen(*reinterpret_cast<const unsigned *>(p)); }
+    __device__ __forceinline__ static float2 load(rsrc_t r, unsigned voff, unsigned soff) {
+        return widen(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
     }
     template <bool NT>
     __device__ __forceinline__ static void store(T *p, float2 v) {
-        // round to nearest even (the conversion's default rounding mode)
-        const unsigned short lo = __builtin_bit_cast(unsigned short, (_Float16)v.x);
-        const unsigned short hi = __builtin_bit_cast(unsigned short, (_Float16)v.y);
-        const unsigned int bits = (unsigned int)lo | ((unsigned int)hi << 16);
         if constexpr (NT) {
-            __builtin_nontemporal_store(bits, reinterpret_cast<unsigned int *>(p));
+            __builtin_nontemporal_store(narrow(v), reinterpret_cast<unsigned int *>(p));
         } else {
-            *reinterpret_cast<unsigned int *>(p) = bits;
+            *reinterpret_cast<unsigned int *>(p) = narrow(v);
         }
+    }
+    template <bool NT>
+    __device__ __forceinline__ static void store(rsrc_t r, unsigned voff, unsigned soff, float2 v) {
+        __builtin_amdgcn_raw_buffer_store_b32(narrow(v), r, voff, soff, NT ? kNtAux : 0);
     }
 };
 

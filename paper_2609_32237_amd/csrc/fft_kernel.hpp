@@ -45,6 +45,7 @@ namespace mi355fft {
 
 enum { XCHG_FULL = 0, XCHG_SPLIT = 1 };
 
+
 template <int... Rs>
 struct Radices {};
 
@@ -59,9 +60,11 @@ struct RadProd<Radices<R, Rs...>> {
     static constexpr int value = R * RadProd<Radices<Rs...>>::value;
 };
 
-template <int N_, int P_, int C_, bool COLS_, int XCHG_, int TWMODE_, bool PERSIST_, class Rad_>
+template <int N_, int P_, int C_, bool COLS_, int XCHG_, int TWMODE_, bool PERSIST_, class Rad_, bool NTROW_ = true>
 struct KCfg {
     static constexpr int N = N_, P = P_, T = N_ / P_, C = C_, THREADS = T * C;
+    // rows of the plain transform are stored with the non-temporal hint
+    static constexpr bool NTROW = NTROW_;
     static constexpr int LOG_T = ilog2(T), LOG_C = ilog2(C);
     static constexpr bool COLS = COLS_, PERSIST = PERSIST_;
     static constexpr int XCHG = XCHG_, TWMODE = TWMODE_;
@@ -307,28 +310,60 @@ __device__ __forceinline__ long long logical_block(int xcd_remap) {
     return xcd < rem ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
 }
 
+// Global access of the P points of transform c of logical block blk (the
+// caller guarantees the block exists).  With buffer addressing the workgroup's
+// base is uniform, each lane adds one 32-bit offset and each register a
+// scalar one; every access stays inside the resource's span, which the host
+// checked fits 31 bits.  Lanes of transforms past the end of the batch read
+// transform 0 of their block instead (in bounds, never stored), so the loads
+// need no per-lane predication.
 template <class K, int ST>
-__device__ __forceinline__ void load_points(float2 (&v)[K::P], const void *__restrict__ in, long long base,
-                                            long long stride, int t, bool valid) {
-    using T = typename Store<ST>::T;
-    const T *src = reinterpret_cast<const T *>(in) + base;
-    static_for<0, K::P>([&](auto ic) {
-        constexpr int i = decltype(ic)::value;
-        const long long pos = t + K::T * i;
-        v[i] = valid ? Store<ST>::load(src + (K::COLS ? pos * stride : pos)) : make_float2(0.f, 0.f);
-    });
+__device__ __forceinline__ void load_points(float2 (&v)[K::P], const void *__restrict__ in, long long blk, int c,
+                                            int t, bool valid, const KArgs &a) {
+    constexpr int EL = Store<ST>::BYTES;
+    const int cl = valid ? c : 0;
+    if (!a.wide) {
+        const char *base = reinterpret_cast<const char *>(in) + blk * K::C * a.in_dist * EL;
+        const rsrc_t r = make_rsrc(base, a.in_span);
+        const unsigned lane = (unsigned)((cl * a.in_dist + (long long)t * a.stride) * EL);
+        static_for<0, K::P>([&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            const unsigned soff = (unsigned)((long long)(K::T * i) * a.stride * EL);
+            v[i] = Store<ST>::load(r, lane, soff);
+        });
+    } else {
+        using T = typename Store<ST>::T;
+        const T *src = reinterpret_cast<const T *>(in) + (blk * K::C + cl) * a.in_dist;
+        static_for<0, K::P>([&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            const long long pos = t + K::T * i;
+            v[i] = Store<ST>::load(src + pos * a.stride);
+        });
+    }
 }
 
 template <class K, int ST, bool NT>
-__device__ __forceinline__ void store_points(const float2 (&v)[K::P], void *__restrict__ out, long long base,
-                                             long long stride, int t) {
-    using T = typename Store<ST>::T;
-    T *dst = reinterpret_cast<T *>(out) + base;
-    static_for<0, K::P>([&](auto ic) {
-        constexpr int i = decltype(ic)::value;
-        const long long pos = t + K::T * i;
-        Store<ST>::template store<NT>(dst + (K::COLS ? pos * stride : pos), v[i]);
-    });
+__device__ __forceinline__ void store_points(const float2 (&v)[K::P], void *__restrict__ out, long long blk, int c,
+                                             int t, const KArgs &a) {
+    constexpr int EL = Store<ST>::BYTES;
+    if (!a.wide) {
+        char *base = reinterpret_cast<char *>(out) + blk * K::C * a.out_dist * EL;
+        const rsrc_t r = make_rsrc(base, a.out_span);
+        const unsigned lane = (unsigned)((c * a.out_dist + (long long)t * a.stride) * EL);
+        static_for<0, K::P>([&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            const unsigned soff = (unsigned)((long long)(K::T * i) * a.stride * EL);
+            Store<ST>::template store<NT>(r, lane, soff, v[i]);
+        });
+    } else {
+        using T = typename Store<ST>::T;
+        T *dst = reinterpret_cast<T *>(out) + (blk * K::C + c) * a.out_dist;
+        static_for<0, K::P>([&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            const long long pos = t + K::T * i;
+            Store<ST>::template store<NT>(dst + pos * a.stride, v[i]);
+        });
+    }
 }
 
 // The whole on-chip computation of one transform (first exchange of the
@@ -368,35 +403,36 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
                                                          const float2 *__restrict__ tw,
                                                          const float2 *__restrict__ spec, KArgs a) {
     __shared__ float lds[K::LDS_FLOATS];
-    // the range-compression pass writes the intermediate image the azimuth
-    // pass reads next: keep it cacheable; every other output streams out
-    constexpr bool NT = !(EPI == EPI_MATCHED && !K::COLS);
+    // Streaming (non-temporal) stores only where each workgroup writes whole
+    // cache lines: contiguous rows.  A column workgroup writes C-element pieces
+    // of each line, which L2 must merge with its neighbours' pieces; and the
+    // range-compression pass writes the intermediate the azimuth pass reads
+    // next, which should stay cacheable.
+    constexpr bool NT = K::NTROW && !K::COLS && EPI == EPI_NONE;
     const int tid = threadIdx.x;
     const int c = K::COLS ? (tid & (K::C - 1)) : (tid >> K::LOG_T);
     const int t = K::COLS ? (tid >> K::LOG_C) : (tid & (K::T - 1));
     float2 v[K::P];
     if constexpr (!K::PERSIST) {
-        const long long b = logical_block(a.xcd_remap) * K::C + c;
-        const bool valid = b < a.batch;
-        load_points<K, IN_ST>(v, in, valid ? b * a.in_dist : 0, a.stride, t, valid);
+        const long long blk = logical_block(a.xcd_remap);
+        const bool valid = blk * K::C + c < a.batch;
+        load_points<K, IN_ST>(v, in, blk, c, t, valid, a);
         transform<K, INV, EPI, true>(v, t, c, tw, spec, a.scale, lds);
-        if (valid) store_points<K, OUT_ST, NT>(v, out, b * a.out_dist, a.stride, t);
+        if (valid) store_points<K, OUT_ST, NT>(v, out, blk, c, t, a);
     } else {
         // persistent: this workgroup takes blocks blockIdx.x, + gridDim.x, ...
         const long long nblk = (a.batch + K::C - 1) / K::C;
         long long blk = blockIdx.x;
-        long long b = blk * K::C + c;
-        bool valid = b < a.batch;
-        load_points<K, IN_ST>(v, in, valid ? b * a.in_dist : 0, a.stride, t, valid);
+        bool valid = blk * K::C + c < a.batch;
+        load_points<K, IN_ST>(v, in, blk, c, t, valid, a);
         for (; blk < nblk; blk += gridDim.x) {
-            const long long nb = (blk + gridDim.x) * K::C + c;
-            const bool nvalid = nb < a.batch;
+            const long long nblk2 = blk + gridDim.x;
+            const bool nvalid = nblk2 * K::C + c < a.batch;
             float2 nv[K::P];
-            load_points<K, IN_ST>(nv, in, nvalid ? nb * a.in_dist : 0, a.stride, t, nvalid);
+            if (nblk2 < nblk) load_points<K, IN_ST>(nv, in, nblk2, c, t, nvalid, a);  // uniform
             transform<K, INV, EPI, false>(v, t, c, tw, spec, a.scale, lds);
-            if (valid) store_points<K, OUT_ST, NT>(v, out, b * a.out_dist, a.stride, t);
+            if (valid) store_points<K, OUT_ST, NT>(v, out, blk, c, t, a);
             static_for<0, K::P>([&](auto ic) { v[ic] = nv[ic]; });
-            b = nb;
             valid = nvalid;
         }
     }
@@ -405,8 +441,10 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
 // Host-side launcher for one instantiation.  Persistent kernels get as many
 // workgroups as fit on the device at once (never more than there is work).
 template <class K, int IN_ST, int OUT_ST, bool INV, int EPI>
-hipError_t launch_one(const void *in, void *out, const float2 *tw, const float2 *spec, const KArgs &a,
+hipError_t launch_one(const void *in, void *out, const float2 *tw, const float2 *spec, const KArgs &args,
                       hipStream_t stream) {
+    KArgs a = args;
+    set_spans(a, K::N, K::C, Store<IN_ST>::BYTES, Store<OUT_ST>::BYTES);
     long long blocks = (a.batch + K::C - 1) / K::C;
     if (blocks <= 0 || blocks > 0x7fffffffLL) return hipErrorInvalidValue;
     auto kern = fft_kernel<K, IN_ST, OUT_ST, INV, EPI>;

@@ -16,7 +16,24 @@ struct KArgs {
     long long out_dist;  // elements between transform starts in the output
     float scale;         // epilogue scale
     int xcd_remap;       // 1: map blocks so consecutive strips share an XCD
+    int wide;            // 1: 64-bit pointer addressing (span or sign does not fit buffer offsets)
+    unsigned in_span;    // bytes one workgroup's input occupies (buffer addressing)
+    unsigned out_span;   // bytes one workgroup's output occupies
 };
+
+// Fills the addressing fields of `a` for workgroups of `c` transforms of `n`
+// points with elements of in_bytes / out_bytes.
+inline void set_spans(KArgs &a, long long n, long long c, int in_bytes, int out_bytes) {
+    const long long lim = 0x7fffffffLL;
+    const long long cc = c < a.batch ? c : a.batch;
+    const long long in_el = (cc - 1) * a.in_dist + (n - 1) * a.stride + 1;
+    const long long out_el = (cc - 1) * a.out_dist + (n - 1) * a.stride + 1;
+    const bool ok = a.in_dist >= 0 && a.out_dist >= 0 && a.stride >= 1 && in_el * in_bytes <= lim &&
+                    out_el * out_bytes <= lim;
+    a.wide = ok ? 0 : 1;
+    a.in_span = ok ? (unsigned)(in_el * in_bytes) : 0u;
+    a.out_span = ok ? (unsigned)(out_el * out_bytes) : 0u;
+}
 
 // Each returns the launch status (hipErrorInvalidValue for an unsupported
 // combination of layout, storages, direction and epilogue, or a variant index
