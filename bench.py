@@ -58,14 +58,18 @@ def gflops(n, batch, seconds):
 
 
 class Flusher:
-    """Writes a 1 GiB buffer on the current stream: evicts the 256 MiB Infinity
-    Cache and every L2 before a cache-cold sample (Section III's cold runs)."""
+    """Reads a 1 GiB buffer on the current stream: evicts the 256 MiB Infinity
+    Cache and every L2 before a cache-cold sample (Section III's cold runs).
+    A read leaves clean lines behind; a write-based flush would leave dirty
+    lines whose write-back lands inside the next timed call."""
 
     def __init__(self, torch):
-        self.buf = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+        self.buf = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        self.acc = torch.empty((), dtype=torch.float32, device="cuda")
+        self.torch = torch
 
     def __call__(self):
-        self.buf.fill_(1.0)
+        self.torch.sum(self.buf, dim=0, out=self.acc)
 
 
 def time_samples(torch, fn, flush, samples, warmup=2):
