@@ -1,4 +1,4 @@
-"""fp64 CPU oracle for the batched FFT and the SAR chain -- TEST INFRASTRUCTURE.
+"""fp64 CPU oracle for the batched FFT and the SAR chains -- TEST INFRASTRUCTURE.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may import this package.  The product library never calls it and
@@ -43,7 +43,10 @@ def _load():
     lib.oracle_fft.argtypes = [i64, i64, i64, i64, ip, dp, dp, ip]
     lib.oracle_sar_chain.argtypes = [i64, i64, dp, dp, dp, dp, ip]
     lib.oracle_xcorr2d_points.argtypes = [i64, i64, dp, dp, dp, i64, dp, dp, dp]
-    for f in (lib.oracle_dft_direct, lib.oracle_fft, lib.oracle_sar_chain, lib.oracle_xcorr2d_points):
+    lib.oracle_rd_chain.argtypes = [i64, i64, dp, dp, dp, ip, dp, ip]
+    lib.oracle_rd_interp_table.argtypes = [dp]
+    for f in (lib.oracle_dft_direct, lib.oracle_fft, lib.oracle_sar_chain, lib.oracle_xcorr2d_points,
+              lib.oracle_rd_chain, lib.oracle_rd_interp_table):
         f.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -138,4 +141,37 @@ def xcorr2d_points(raw, range_ref, az_ref, pts_az, pts_rg) -> np.ndarray:
     rc = _load().oracle_xcorr2d_points(n_az, n_rg, _ptr(raw), _ptr(hr), _ptr(ha), pa.size,
                                        _ptr(pa), _ptr(pr), _ptr(out))
     _check(rc, "xcorr2d_points")
+    return out
+
+
+RD_TAPS = 8
+RD_SUB = 128
+GEOMETRY_KEYS = ("wavelength", "speed", "prf", "range_bin", "r_near")
+
+
+def rd_interp_table() -> np.ndarray:
+    """The range-cell migration interpolator's table, (RD_SUB + 1, RD_TAPS)."""
+    tab = np.empty((RD_SUB + 1, RD_TAPS), dtype=np.float64)
+    _check(_load().oracle_rd_interp_table(_ptr(tab)), "rd_interp_table")
+    return tab
+
+
+def rd_chain(raw, range_ref, geometry: dict, stop_after: int = 5, nthreads: int | None = None) -> np.ndarray:
+    """The full range-Doppler chain on an (n_az, n_rg) echo (rows = pulses).
+
+    ``geometry`` holds wavelength [m], speed [m/s], prf [Hz], range_bin [m]
+    (slant-range spacing of the range samples) and r_near [m] (slant range of
+    range bin 0).  ``stop_after`` returns the image after step 1 (range
+    compression), 2 (azimuth FFT / n_az), 3 (RCMC), 4 (azimuth filter) or 5
+    (azimuth inverse FFT: the focused image)."""
+    raw = _c128(raw)
+    n_az, n_rg = raw.shape
+    hr = _c128(range_ref).reshape(-1)
+    if hr.size != n_rg:
+        raise ValueError("range reference length must match the range axis")
+    geo = np.array([float(geometry[k]) for k in GEOMETRY_KEYS], dtype=np.float64)
+    out = np.empty_like(raw)
+    rc = _load().oracle_rd_chain(n_az, n_rg, _ptr(raw), _ptr(hr), _ptr(geo), int(stop_after), _ptr(out),
+                                 nthreads or default_threads())
+    _check(rc, "rd_chain")
     return out

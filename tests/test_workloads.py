@@ -85,3 +85,31 @@ def test_sar_scene_noise_level():
     quiet = sc.raw[200:, 200:]  # far from the single echo
     np.testing.assert_allclose(quiet.real.std(), 0.01, rtol=0.05)
     np.testing.assert_allclose(quiet.imag.std(), 0.01, rtol=0.05)
+
+
+def test_rd_scene_matches_the_papers_geometry():
+    """Section X: 600 m synthetic aperture (1500 pulses at 500 Hz) at 20 km,
+    about 1.8 range bins of migration across it, 1200-sample pulses, every
+    echo inside the frame; deterministic for a seed."""
+    sc = workloads.rd_scene(sigma=0.0)
+    g, p = sc.geometry, sc.params
+    assert g["range_bin"] == pytest.approx(299_792_458.0 / 240e6)
+    r0 = 20_000.0
+    aperture = g["wavelength"] * r0 / p["antenna"]
+    assert aperture == pytest.approx(600.0)
+    assert aperture / g["speed"] * g["prf"] == pytest.approx(1500.0)
+    migration = (np.hypot(r0, aperture / 2) - r0) / g["range_bin"]
+    assert 1.7 < migration < 1.9
+    assert p["pulse_samples"] == 1200 and np.count_nonzero(sc.range_ref) == 1200
+    assert len(sc.targets_az) == 6
+    # a lone target's echo is lit on its aperture only (about 1360-1580 pulses)
+    for a_i, n_i, _ in workloads.RD_TARGETS:
+        lone = workloads.rd_scene(sigma=0.0, targets=((a_i, n_i, 1.0),))
+        r0_i = g["r_near"] + n_i * g["range_bin"]
+        half = g["wavelength"] * r0_i / (2 * p["antenna"]) * g["prf"] / g["speed"]
+        lit = np.nonzero(abs(lone.raw[:, n_i + 600]) > 0.5)[0]
+        assert abs(lit.min() - (a_i - half)) <= 1 and abs(lit.max() - (a_i + half)) <= 1
+    noisy = workloads.rd_scene_small()
+    again = workloads.rd_scene_small()
+    assert np.array_equal(noisy.raw, again.raw)
+    assert noisy.raw.dtype == np.complex64 and noisy.range_ref.dtype == np.complex64

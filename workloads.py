@@ -195,3 +195,118 @@ def sar_scene(
         amplitudes=amp,
         params=params,
     )
+
+
+# --------------------------------------------------------------------------
+# Range-Doppler scene: the paper's L-band stripmap geometry
+# --------------------------------------------------------------------------
+
+SPEED_OF_LIGHT = 299_792_458.0
+
+# Six point targets as (pulse of closest approach, range bin of closest
+# approach, amplitude): spread over the frame so that every synthetic
+# aperture (about 1500 pulses) and every echo (1200 samples plus 2 bins of
+# migration) lies inside it.
+RD_TARGETS = ((1024, 512, 1.0), (1024, 2304, 1.0), (2048, 1280, 1.0),
+              (2048, 2816, 1.0), (3072, 256, 1.0), (3072, 1792, 1.0))
+
+
+@dataclass
+class RdScene:
+    """Simulated stripmap echo, the transmitted pulse replica and the geometry."""
+
+    raw: np.ndarray  # (n_az, n_rg) complex64, rows = pulses
+    range_ref: np.ndarray  # (n_rg,) complex64, the pulse replica from index 0
+    geometry: dict  # wavelength, speed, prf, range_bin, r_near (the processor's inputs)
+    targets_az: np.ndarray  # (K,) int64 pulse of closest approach
+    targets_rg: np.ndarray  # (K,) int64 range bin of closest approach
+    amplitudes: np.ndarray  # (K,) float64
+    params: dict = field(default_factory=dict)
+
+
+def rd_scene(
+    n_az: int = 4096,
+    n_rg: int = 4096,
+    wavelength: float = 0.24,
+    bandwidth: float = 100e6,
+    fs: float = 120e6,
+    speed: float = 200.0,
+    prf: float = 500.0,
+    antenna: float = 8.0,
+    pulse_samples: int = 1200,
+    r_near: float = 17500.0,
+    targets=RD_TARGETS,
+    sigma: float = 0.01,
+    seed: int = 5,
+) -> RdScene:
+    """Stripmap echo of point targets (paper, Section X: lambda 0.24 m,
+    B 100 MHz, fs 120 MHz, v 200 m/s, PRF 500 Hz, 8 m antenna, six targets and
+    complex Gaussian noise; the pulse lasts ``pulse_samples`` samples).
+
+    Broadside geometry, start-stop approximation.  Pulse a is sent at slow time
+    a / PRF; target i is closest at pulse a_i, at slant range
+    R0_i = r_near + n_i * dr with dr = c / (2 fs) the range bin spacing, so
+    R_i(a) = sqrt(R0_i^2 + (v (a - a_i) / PRF)^2).  The antenna beam (width
+    lambda / L) lights the target while |v (a - a_i) / PRF| <= lambda R0_i / (2L),
+    which is its synthetic aperture (600 m at 20 km).  Range sample m is taken
+    at fast time tau_m = 2 r_near / c + m / fs, and the baseband echo is
+
+        A_i p(tau_m - 2 R_i(a) / c) exp(-j 4 pi R_i(a) / lambda),
+
+    with p(u) = exp(j pi K (u - T/2)^2) for 0 <= u < T (T = pulse_samples / fs,
+    K = B / T: an up-chirp spanning -B/2 .. B/2) and zero elsewhere.  The
+    replica is p sampled at m / fs, m = 0 .. pulse_samples - 1.  The echo is
+    summed in complex128, noise (re and im each normal with standard deviation
+    ``sigma``, from ``default_rng(seed)``) added, and cast once to complex64.
+    """
+    dr = SPEED_OF_LIGHT / (2.0 * fs)
+    t_p = pulse_samples / fs
+    k_r = bandwidth / t_p
+    raw = np.zeros((n_az, n_rg), dtype=np.complex128)
+    ta = np.array([t[0] for t in targets], dtype=np.int64)
+    tr = np.array([t[1] for t in targets], dtype=np.int64)
+    amp = np.array([t[2] for t in targets], dtype=np.float64)
+    m_all = np.arange(n_rg, dtype=np.float64)
+    for a_i, n_i, amp_i in zip(ta, tr, amp):
+        r0 = r_near + n_i * dr
+        half = wavelength * r0 / (2.0 * antenna)
+        a_lo = int(np.ceil(a_i - half * prf / speed))
+        a_hi = int(np.floor(a_i + half * prf / speed))
+        if a_lo < 0 or a_hi >= n_az:
+            raise ValueError("a target's synthetic aperture leaves the frame")
+        pulses = np.arange(a_lo, a_hi + 1)
+        x = speed * (pulses - a_i) / prf
+        r = np.sqrt(r0 * r0 + x * x)
+        delay = (r - r_near) / dr  # echo start in (fractional) range samples
+        lo = int(np.floor(delay.min()))
+        hi = int(np.ceil(delay.max())) + pulse_samples + 1
+        if lo < 0 or hi > n_rg:
+            raise ValueError("a target's echo leaves the range window")
+        m = m_all[lo:hi]
+        u = (m[None, :] - delay[:, None]) / fs
+        inside = (u >= 0.0) & (u < t_p)
+        echo = np.where(inside, np.exp(1j * np.pi * k_r * (u - t_p / 2) ** 2), 0.0)
+        echo *= (amp_i * np.exp(-4j * np.pi * r / wavelength))[:, None]
+        raw[a_lo:a_hi + 1, lo:hi] += echo
+    if sigma > 0:
+        rng = np.random.default_rng(seed)
+        noise = rng.normal(0.0, sigma, size=(n_az, n_rg, 2))
+        raw += noise[..., 0] + 1j * noise[..., 1]
+    u = np.arange(pulse_samples) / fs
+    ref = np.zeros(n_rg, dtype=np.complex128)
+    ref[:pulse_samples] = np.exp(1j * np.pi * k_r * (u - t_p / 2) ** 2)
+    geometry = dict(wavelength=wavelength, speed=speed, prf=prf, range_bin=dr, r_near=r_near)
+    params = dict(n_az=n_az, n_rg=n_rg, bandwidth=bandwidth, fs=fs, antenna=antenna,
+                  pulse_samples=pulse_samples, sigma=sigma, seed=seed, **geometry)
+    return RdScene(raw=raw.astype(np.complex64), range_ref=ref.astype(np.complex64), geometry=geometry,
+                   targets_az=ta, targets_rg=tr, amplitudes=amp, params=params)
+
+
+def rd_scene_small(**kw) -> RdScene:
+    """A 1024 x 1024 version of the same scene for quick checks: PRF 125 Hz
+    keeps the 600 m aperture (375 pulses) and the 1.8-bin migration, and a
+    300-sample (2.5 us) pulse fits the shorter range window."""
+    args = dict(n_az=1024, n_rg=1024, prf=125.0, pulse_samples=300,
+                targets=((256, 128, 1.0), (512, 640, 1.0), (768, 384, 1.0), (768, 700, 0.7)))
+    args.update(kw)
+    return rd_scene(**args)
