@@ -10,7 +10,11 @@
  *     compression (FFT, matched filter, inverse FFT, 1/N_r) fused in one pass,
  *     then the azimuth FFT read straight from the columns with its 1/N_a
  *     scale, the azimuth matched filter and the azimuth inverse FFT fused in a
- *     second pass (Section X).
+ *     second pass (Section X);
+ *   - the paper's full range-Doppler chain with range-cell migration
+ *     correction and the baseband azimuth filter (Section X): range
+ *     compression, the azimuth FFT, and one fused pass that interpolates,
+ *     filters and inverse-transforms each range bin.
  *
  * Conventions shared by every entry point
  *   - Complex values are interleaved (re, im): FP32 storage is two floats
@@ -155,6 +159,82 @@ int sar_form_image_ex(int64_t n_az, int64_t n_rg, int inter_storage, const void 
  */
 int sar_form_image(const void *raw, const void *range_ref, const void *az_ref, void *out,
                    hipStream_t stream);
+
+/*
+ * Acquisition geometry of a broadside stripmap echo (Section X's scene: an
+ * L-band platform flying straight at constant speed, zero squint).
+ */
+typedef struct sar_geometry {
+    double wavelength; /* carrier wavelength lambda [m], > 0 */
+    double speed;      /* platform speed v [m/s], > 0 */
+    double prf;        /* pulse repetition frequency [Hz], > 0 */
+    double range_bin;  /* slant-range spacing of the range samples, c / (2 fs) [m], > 0 */
+    double r_near;     /* slant range of range sample 0 [m], > 0 */
+} sar_geometry;
+
+/*
+ * sar_rd_workspace_bytes -- device workspace sar_rd_form_image needs: the
+ * range reference spectrum, the per-Doppler-bin and per-range-bin tables of
+ * the migration correction and azimuth filter, the interpolator table and
+ * one intermediate image (the range-Doppler image, stored one row per range
+ * bin: n_az * n_rg * 8 bytes for FP32, * 4 for FP16), each part 256-byte
+ * aligned.  Returns 0 for an invalid or unsupported request.
+ */
+size_t sar_rd_workspace_bytes(int64_t n_az, int64_t n_rg, int inter_storage);
+
+/*
+ * sar_rd_form_image -- focused image of a stripmap echo by the full
+ * range-Doppler algorithm of Section X, in three passes over device memory.
+ *
+ *   n_az, n_rg      pulses (rows) and range samples (columns); each a power of
+ *                   two in [1024, 16384] with n_az * n_rg <= 2^27, else
+ *                   FFT_EUNSUPPORTED.
+ *   inter_storage   FFT_STORAGE_FP32 or FFT_STORAGE_FP16 for the stored
+ *                   intermediate (Section X: FP16 with the fixed-shift
+ *                   scaling 1/N_r in range compression and 1/N_a on the
+ *                   azimuth FFT output).
+ *   geo             host pointer to the acquisition geometry; every field
+ *                   finite and > 0, and lambda * prf / (4 v) < 1 (the largest
+ *                   Doppler frequency, prf / 2, has a real D), else
+ *                   FFT_EINVAL.  lambda * prf / (4 v) must also be at most
+ *                   1/3, else FFT_EUNSUPPORTED: the migration-correction pass
+ *                   shares one window of rows across strips of up to 16
+ *                   range bins, whose shifts must then differ by less than a
+ *                   bin (the scene of Section X has 0.15).  Read before the
+ *                   call returns.
+ *   raw             n_az x n_rg complex FP32 echo, row-major, rows = pulses.
+ *   range_ref       n_rg complex FP32: the transmitted pulse replica,
+ *                   starting at index 0 (zero beyond the pulse).
+ *   out             n_az x n_rg complex FP32 focused image (rows = pulses,
+ *                   columns = range bins); must not overlap raw or the
+ *                   workspace.  Also holds the range-compressed image between
+ *                   the first two passes.
+ *   workspace       sar_rd_workspace_bytes(n_az, n_rg, inter_storage) bytes,
+ *                   256-byte aligned; contents on entry are ignored.
+ *   stream          HIP stream; five kernels run on it in order (tables,
+ *                   reference spectrum, three passes).
+ *
+ * Computes, in Section X's order:
+ *   1. y[a, :] = IFFT( FFT(raw[a, :]) * conj(FFT(range_ref)) ) / n_rg;
+ *   2. Z[:, n] = FFT(y[:, n]) / n_az  (Doppler bin k has frequency
+ *      f_k = k prf / n_az, minus prf for k >= n_az / 2);
+ *   3. range-cell migration correction: with D_k = sqrt(1 - (lambda f_k /
+ *      2v)^2), R0_n = r_near + n range_bin and dn = R0_n (1/D_k - 1) /
+ *      range_bin, s = floor(dn), mu = dn - s:
+ *        Zr[k, n] = sum_{j=0..7} g_j(mu) Z[k, n + s + j - 3]
+ *      (samples outside [0, n_rg) count as zero), where g(mu) blends
+ *      linearly between the two nearest of 129 rows of an 8-tap
+ *      Kaiser-windowed (beta 2.5) sinc table at mu = q / 128, each row
+ *      normalised to unit sum;
+ *   4. the baseband azimuth filter Zr[k, n] *= exp(+j 4 pi R0_n (D_k - 1) /
+ *      lambda), its phase evaluated in cycles;
+ *   5. out[:, n] = IFFT(Zr[:, n])  (unnormalised).
+ * Returns FFT_OK, FFT_EINVAL, FFT_EUNSUPPORTED, FFT_EALIGN, FFT_ENOMEM or
+ * FFT_EHIP.
+ */
+int sar_rd_form_image(int64_t n_az, int64_t n_rg, int inter_storage, const sar_geometry *geo,
+                      const void *raw, const void *range_ref, void *out, void *workspace,
+                      hipStream_t stream);
 
 /* fft_strerror -- static description of a return code (never NULL). */
 const char *fft_strerror(int code);

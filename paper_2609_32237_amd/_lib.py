@@ -26,7 +26,15 @@ FFT_EHIP = -5
 
 # every symbol include/mi355fft.h declares
 EXPORTS = ("fft_plan_create", "fft_execute", "fft_plan_destroy", "sar_workspace_bytes",
-           "sar_form_image_ex", "sar_form_image", "fft_strerror")
+           "sar_form_image_ex", "sar_form_image", "sar_rd_workspace_bytes", "sar_rd_form_image",
+           "fft_strerror")
+
+
+class SarGeometry(ctypes.Structure):
+    """struct sar_geometry: broadside stripmap acquisition (metres, Hz, m/s)."""
+
+    _fields_ = [("wavelength", ctypes.c_double), ("speed", ctypes.c_double), ("prf", ctypes.c_double),
+                ("range_bin", ctypes.c_double), ("r_near", ctypes.c_double)]
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(
@@ -47,6 +55,10 @@ lib.sar_form_image_ex.argtypes = [_i64, _i64, _int, _vp, _vp, _vp, _vp, _vp, _vp
 lib.sar_form_image_ex.restype = _int
 lib.sar_form_image.argtypes = [_vp, _vp, _vp, _vp, _vp]
 lib.sar_form_image.restype = _int
+lib.sar_rd_workspace_bytes.argtypes = [_i64, _i64, _int]
+lib.sar_rd_workspace_bytes.restype = ctypes.c_size_t
+lib.sar_rd_form_image.argtypes = [_i64, _i64, _int, ctypes.POINTER(SarGeometry), _vp, _vp, _vp, _vp, _vp]
+lib.sar_rd_form_image.restype = _int
 lib.fft_strerror.argtypes = [_int]
 lib.fft_strerror.restype = ctypes.c_char_p
 
@@ -94,3 +106,21 @@ def sar_form_image_ex(n_az: int, n_rg: int, inter_storage: int, raw: int, range_
 
 def sar_form_image(raw: int, range_ref: int, az_ref: int, out: int, stream: int = 0) -> None:
     _check(lib.sar_form_image(raw, range_ref, az_ref, out, stream), "sar_form_image")
+
+
+def sar_rd_workspace_bytes(n_az: int, n_rg: int, inter_storage: int) -> int:
+    return int(lib.sar_rd_workspace_bytes(n_az, n_rg, inter_storage))
+
+
+def geometry(g) -> SarGeometry:
+    """A SarGeometry from a mapping with the struct's field names (or itself)."""
+    if isinstance(g, SarGeometry):
+        return g
+    return SarGeometry(*(float(g[k]) for k, _ in SarGeometry._fields_))
+
+
+def sar_rd_form_image(n_az: int, n_rg: int, inter_storage: int, geo, raw: int, range_ref: int, out: int,
+                      workspace: int, stream: int = 0) -> None:
+    g = geometry(geo)
+    _check(lib.sar_rd_form_image(n_az, n_rg, inter_storage, ctypes.byref(g), raw, range_ref, out, workspace,
+                                 stream), "sar_rd_form_image")

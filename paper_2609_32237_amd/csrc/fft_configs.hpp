@@ -35,6 +35,8 @@ struct Configs<1024> {
                        KCfg<1024, 16, 4, false, XCHG_FULL, 0, false, Radices<16, 16, 4>>>;
     using Cols = KList<KCfg<1024, 16, 8, true, XCHG_SPLIT, 1, false, Radices<16, 16, 4>>,
                        KCfg<1024, 16, 8, true, XCHG_FULL, 0, false, Radices<16, 16, 4>>>;
+    using Rcmc = KList<KCfg<1024, 16, 16, false, XCHG_SPLIT, 1, false, Radices<16, 16, 4>>,
+                       KCfg<1024, 16, 8, false, XCHG_SPLIT, 1, false, Radices<16, 16, 4>>>;
     static constexpr int kRowDefault[2] = {1, 0}, kColDefault[2] = {0, 0};
     static constexpr int kRowMatched = 1, kColMatched = 0;
 };
@@ -46,6 +48,8 @@ struct Configs<2048> {
                        KCfg<2048, 16, 2, false, XCHG_FULL, 0, false, Radices<16, 16, 8>>>;
     using Cols = KList<KCfg<2048, 16, 4, true, XCHG_SPLIT, 1, false, Radices<16, 16, 8>>,
                        KCfg<2048, 16, 4, true, XCHG_FULL, 0, false, Radices<16, 16, 8>>>;
+    using Rcmc = KList<KCfg<2048, 16, 8, false, XCHG_SPLIT, 1, false, Radices<16, 16, 8>>,
+                       KCfg<2048, 16, 4, false, XCHG_SPLIT, 1, false, Radices<16, 16, 8>>>;
     static constexpr int kRowDefault[2] = {0, 0}, kColDefault[2] = {0, 0};
     static constexpr int kRowMatched = 0, kColMatched = 0;
 };
@@ -64,6 +68,8 @@ struct Configs<4096> {
                        KCfg<4096, 32, 8, true, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>>;
     // plain columns: 8-column strips measured fastest (2.3 vs 1.7 TB/s); the
     // matched-filter column pass spills with them and keeps 4-column strips
+    using Rcmc = KList<KCfg<4096, 32, 8, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>,
+                       KCfg<4096, 16, 4, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>>;
     static constexpr int kRowDefault[2] = {0, 1}, kColDefault[2] = {3, 3};
     static constexpr int kRowMatched = 1, kColMatched = 0;
 };
@@ -75,6 +81,8 @@ struct Configs<8192> {
                        KCfg<8192, 16, 1, false, XCHG_FULL, 0, false, Radices<16, 16, 16, 2>>>;
     using Cols = KList<KCfg<8192, 32, 2, true, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 2>>,
                        KCfg<8192, 32, 2, true, XCHG_SPLIT, 0, false, Radices<16, 16, 16, 2>>>;
+    using Rcmc = KList<KCfg<8192, 32, 4, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 2>>,
+                       KCfg<8192, 16, 2, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 2>>>;
     static constexpr int kRowDefault[2] = {0, 0}, kColDefault[2] = {0, 0};
     static constexpr int kRowMatched = 0, kColMatched = 0;
 };
@@ -87,6 +95,8 @@ struct Configs<16384> {
     using Cols = KList<KCfg<16384, 32, 1, true, XCHG_SPLIT, 0, false, Radices<16, 16, 16, 4>>,
                        KCfg<16384, 32, 1, true, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 4>>>;
     static constexpr int kRowDefault[2] = {1, 0}, kColDefault[2] = {1, 1};
+    using Rcmc = KList<KCfg<16384, 32, 2, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 4>>,
+                       KCfg<16384, 16, 1, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 4>>>;
     static constexpr int kRowMatched = 1, kColMatched = 1;
 };
 
@@ -112,7 +122,12 @@ hipError_t with_variant(int idx, KList<K, Ks...>, F &&f) {
 //   plain FFT:  rows or columns, input storage == output storage, either direction;
 //   matched:    forward, multiply by conj(spec) * scale, inverse:
 //               rows read FP32 and write FP32 or FP16 (range compression);
-//               columns read FP32 or FP16 and write FP32 (azimuth compression).
+//               columns read FP32 or FP16 and write FP32 (azimuth compression);
+//   scaled:     columns, forward, input storage == output storage (the azimuth
+//               FFT of the full range-Doppler chain);
+//   RCMC:       the Rcmc list (row-mapped, several transforms per workgroup),
+//               inverse, read FP32 or FP16, write FP32 columns (migration
+//               correction, azimuth filter and azimuth inverse FFT).
 template <class K>
 hipError_t dispatch_cfg(int in_st, int out_st, int inv, int epi, const void *in, void *out, const float2 *tw,
                         const float2 *spec, const KArgs &a, hipStream_t s) {
@@ -124,6 +139,16 @@ hipError_t dispatch_cfg(int in_st, int out_st, int inv, int epi, const void *in,
         return inv ? launch_one<K, 1, 1, true, EPI_NONE>(in, out, tw, spec, a, s)
                    : launch_one<K, 1, 1, false, EPI_NONE>(in, out, tw, spec, a, s);
     }
+    if (epi == EPI_SCALE) {
+        if constexpr (K::COLS && !K::PERSIST) {
+            if (inv || in_st != out_st) return hipErrorInvalidValue;
+            return in_st == 0 ? launch_one<K, 0, 0, false, EPI_SCALE>(in, out, tw, spec, a, s)
+                              : launch_one<K, 1, 1, false, EPI_SCALE>(in, out, tw, spec, a, s);
+        } else {
+            return hipErrorInvalidValue;
+        }
+    }
+    if (epi == EPI_RCMC) return hipErrorInvalidValue;  // only through dispatch_rcmc
     if (epi != EPI_MATCHED || inv) return hipErrorInvalidValue;
     if constexpr (!K::COLS) {
         if (in_st != 0) return hipErrorInvalidValue;
@@ -136,10 +161,23 @@ hipError_t dispatch_cfg(int in_st, int out_st, int inv, int epi, const void *in,
     }
 }
 
+template <class K>
+hipError_t dispatch_rcmc(int in_st, int out_st, int inv, const void *in, void *out, const float2 *tw,
+                         const float2 *spec, const KArgs &a, hipStream_t s) {
+    if (!inv || out_st != 0) return hipErrorInvalidValue;
+    return in_st == 0 ? launch_one<K, 0, 0, true, EPI_RCMC>(in, out, tw, spec, a, s)
+                      : launch_one<K, 1, 0, true, EPI_RCMC>(in, out, tw, spec, a, s);
+}
+
 template <int N>
 hipError_t dispatch(int variant, int layout, int in_st, int out_st, int inv, int epi, const void *in, void *out,
                     const float2 *tw, const float2 *spec, const KArgs &a, hipStream_t s) {
     auto f = [&](auto k) { return dispatch_cfg<decltype(k)>(in_st, out_st, inv, epi, in, out, tw, spec, a, s); };
+    if (layout == LAYOUT_RCMC) {
+        if (epi != EPI_RCMC) return hipErrorInvalidValue;
+        auto g = [&](auto k) { return dispatch_rcmc<decltype(k)>(in_st, out_st, inv, in, out, tw, spec, a, s); };
+        return with_variant(variant >= 0 ? variant : 0, typename Configs<N>::Rcmc{}, g);
+    }
     const int half = (in_st | out_st) != 0;  // any FP16 storage involved
     const bool mf = epi == EPI_MATCHED;
     if (layout == LAYOUT_ROWS) {
@@ -152,8 +190,9 @@ hipError_t dispatch(int variant, int layout, int in_st, int out_st, int inv, int
 
 template <int N>
 int variant_count(int layout) {
-    return layout == LAYOUT_ROWS ? KListSize<typename Configs<N>::Rows>::value
-                                 : KListSize<typename Configs<N>::Cols>::value;
+    return layout == LAYOUT_ROWS   ? KListSize<typename Configs<N>::Rows>::value
+           : layout == LAYOUT_COLS ? KListSize<typename Configs<N>::Cols>::value
+                                   : KListSize<typename Configs<N>::Rcmc>::value;
 }
 
 }  // namespace mi355fft

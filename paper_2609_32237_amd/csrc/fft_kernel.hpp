@@ -71,7 +71,12 @@ struct KCfg {
     // LDS padding: one spare slot every 16 (8-byte exchange) or 32 (4-byte
     // exchange) elements spreads power-of-two strides over the banks.
     static constexpr int PADSH = XCHG_ == XCHG_FULL ? 4 : 5;
-    static constexpr int ROW_SPAN = N_ + (N_ >> PADSH);
+    // Rows of a multi-transform workgroup start RSKEW slots apart modulo the
+    // 32 banks (64 / C four-byte words, or 16 / C eight-byte slots), so that
+    // a read across the C rows of one position (the remapped store below)
+    // spreads over distinct banks.
+    static constexpr int RSKEW = C_ == 1 ? 0 : (XCHG_ == XCHG_FULL ? 16 : 32) / C_;
+    static constexpr int ROW_SPAN = N_ + (N_ >> PADSH) + RSKEW;
     static constexpr int SPAN = COLS_ ? (N_ * C_ + ((N_ * C_) >> PADSH)) : C_ * ROW_SPAN;
     static constexpr int LDS_FLOATS = XCHG_ == XCHG_FULL ? 2 * SPAN : SPAN;
     // Waves per SIMD the LDS allows (a CU has 4 SIMDs and 160 KiB of LDS),
@@ -349,10 +354,10 @@ __device__ __forceinline__ void store_points(const float2 (&v)[K::P], void *__re
     if (!a.wide) {
         char *base = reinterpret_cast<char *>(out) + blk * K::C * a.out_dist * EL;
         const rsrc_t r = make_rsrc(base, a.out_span);
-        const unsigned lane = (unsigned)((c * a.out_dist + (long long)t * a.stride) * EL);
+        const unsigned lane = (unsigned)((c * a.out_dist + (long long)t * a.out_stride) * EL);
         static_for<0, K::P>([&](auto ic) {
             constexpr int i = decltype(ic)::value;
-            const unsigned soff = (unsigned)((long long)(K::T * i) * a.stride * EL);
+            const unsigned soff = (unsigned)((long long)(K::T * i) * a.out_stride * EL);
             Store<ST>::template store<NT>(r, lane, soff, v[i]);
         });
     } else {
@@ -361,9 +366,202 @@ __device__ __forceinline__ void store_points(const float2 (&v)[K::P], void *__re
         static_for<0, K::P>([&](auto ic) {
             constexpr int i = decltype(ic)::value;
             const long long pos = t + K::T * i;
-            Store<ST>::template store<NT>(dst + pos * a.stride, v[i]);
+            Store<ST>::template store<NT>(dst + pos * a.out_stride, v[i]);
         });
     }
+}
+
+// Load stage of the azimuth inverse transform in the range-Doppler chain
+// (Section X: migration correction and azimuth filter fused with the inverse
+// FFT).  The range-Doppler image arrives transposed, one row per range bin
+// (Doppler bin k of range bin m at element m*in_dist + k), so the eight taps
+// of a point are eight neighbouring rows of one column (Section X: gathering
+// eight neighbouring rows).  Thread (t, c) produces Doppler bins
+// k = t + T*i of range bin n = n0 + c (n0 = blk*C) of the corrected,
+// filtered image:
+//   dn = R0_n * (1/D_k - 1) / range_bin, s = floor(dn), mu = dn - s (the
+//   fraction from the shift alone: Section X's fourth fix);
+//   taps g_j = row q + alpha * (row q+1 - row q) of the interpolator table,
+//   q = floor(128 mu), alpha = 128 mu - q (all exact in FP32);
+//   value = sum_j g_j Z[n + s - 3 + j][k];
+//   times exp(+j 2 pi R0_n * 2 (D_k - 1) / lambda), whose phase in cycles is
+//   formed as an unevaluated float sum: the product of the hi parts plus its
+//   exact rounding error (FMA), reduced by its nearest integer (exact), plus
+//   the cross terms; the reduced phase is then accurate to about 1e-7 cycles.
+//
+// The C range bins of the workgroup share their taps: for each Doppler bin k
+// the rows n0 + s0 - 3 .. n0 + s0 + C + 6 (s0 = floor(dn) of range bin n0,
+// never larger than that of the others since dn grows with R0) hold every tap
+// of all C points, as long as dn varies by at most one bin across the strip
+// (the host guarantees it).  Doppler bins are processed in chunks of T (the
+// thread's own k for each i): the workgroup stages the chunk's W >= C + 10
+// rows into LDS (each thread loads W / C of them for its k, one row per load
+// instruction of the wave: contiguous pieces), then each thread reads its
+// eight taps from there.  Two staging buffers alternate, so one barrier per
+// chunk separates writing a buffer from reading it, and the next chunk's
+// loads are in flight while the current one is computed.
+// The image is addressed through one buffer resource spanning its n_rg rows
+// (the host guarantees it fits 31 bits), each row with its own 32-bit offset:
+// rows outside [0, n_rg) fall outside the resource (a negative row wraps to an
+// offset above 2^31, a row past the end lies past the span), and the
+// hardware returns zero for them, which is the value the swath has there.
+template <class K>
+struct RcmcStage {
+    // at least C + 10 rows, rounded up to whole loads per thread (a load
+    // under a lane condition costs the compiler far more than the row)
+    static constexpr int LOADS = (K::C + 10 + K::C - 1) / K::C;  // rows each thread loads
+    static constexpr int W = LOADS * K::C;                        // staged rows per Doppler bin
+    static constexpr int FLOATS = 2 * W * K::T;                   // one buffer, complex
+    // staging pays when the strip shares taps (C >= 4) and two buffers fit
+    static constexpr bool ON = K::C >= 4 && 2 * FLOATS <= K::LDS_FLOATS;
+};
+
+// Point i of thread (t, c): interpolation of the taps z(j) = Z[n + s - 3 + j]
+// with the blended table row, times the azimuth filter.
+template <class K, class TapFn>
+__device__ __forceinline__ float2 rcmc_point(float dn, float2 r0, float4 rw, const float4 *itab, TapFn &&tap) {
+    constexpr int RS = 5;
+    const float fd = floorf(dn);
+    const float qf = (dn - fd) * (float)kRcmcSub;
+    const int q = (int)qf;
+    const float al = qf - (float)q;
+    float2 acc = make_float2(0.0f, 0.0f);
+    static_for<0, 4>([&](auto mc) {
+        constexpr int m = decltype(mc)::value;
+        const float4 g = itab[q * RS + m];
+        const float w0 = fmaf(al, g.y, g.x), w1 = fmaf(al, g.w, g.z);
+        const float2 z0 = tap(2 * m), z1 = tap(2 * m + 1);
+        acc.x = fmaf(w0, z0.x, acc.x);
+        acc.y = fmaf(w0, z0.y, acc.y);
+        acc.x = fmaf(w1, z1.x, acc.x);
+        acc.y = fmaf(w1, z1.y, acc.y);
+    });
+    const float p = r0.x * rw.y;
+    const float e = fmaf(r0.x, rw.y, -p);
+    const float frac = (p - rintf(p)) + (e + fmaf(r0.x, rw.z, r0.y * rw.y));
+    // |frac| <= 1/2 + 2^-20: the hardware sine and cosine take the angle in
+    // revolutions (measured on this range: absolute error below 1.3e-7)
+    const float sn = __builtin_amdgcn_sinf(frac), cs = __builtin_amdgcn_cosf(frac);
+    return make_float2(acc.x * cs - acc.y * sn, acc.x * sn + acc.y * cs);
+}
+
+template <class K, int ST>
+__device__ __forceinline__ void rcmc_load(float2 (&v)[K::P], const void *__restrict__ in, long long blk, int c,
+                                          int t, bool valid, const KArgs &a, const float2 *__restrict__ tables,
+                                          float *lds) {
+    static_assert(!K::COLS && !K::PERSIST, "the migration correction reads rows of the transposed image");
+    static_assert(kRcmcTaps == 8, "four float4 per table row");
+    using S = RcmcStage<K>;
+    constexpr int EL = Store<ST>::BYTES, P = K::P, T = K::T, W = S::W;
+    // table row q holds {g_j, dg_j, g_j+1, dg_j+1} for j = 0, 2, 4, 6 in four
+    // float4 slots of a five-slot stride: consecutive rows start 20 banks
+    // apart, so lanes reading different rows spread over the banks
+    constexpr int RS = 5;
+    __shared__ float4 itab[(kRcmcSub + 1) * RS];
+    const int n_rg = (int)a.batch;
+    const float4 *rows = reinterpret_cast<const float4 *>(tables);
+    const float2 *cols = reinterpret_cast<const float2 *>(reinterpret_cast<const char *>(tables) +
+                                                          rd_tables_layout(K::N, n_rg).cols);
+    const float4 *interp = reinterpret_cast<const float4 *>(reinterpret_cast<const char *>(tables) +
+                                                            rd_tables_layout(K::N, n_rg).interp);
+    for (int e = threadIdx.x; e < (kRcmcSub + 1) * 4; e += K::THREADS) itab[(e >> 2) * RS + (e & 3)] = interp[e];
+    const int n0 = (int)(blk * K::C);
+    const int n = n0 + (valid ? c : 0);  // lanes past the last column redo the block's first
+    const float r00 = cols[n0].x;
+    const float2 r0 = cols[n];
+    const unsigned rb = (unsigned)(a.in_dist * EL);
+    const rsrc_t r = make_rsrc(in, (unsigned)((long long)n_rg * a.in_dist * EL));
+    // integer part of a shift, kept at most n_rg so that no row offset wraps
+    auto shift = [&](float dn) { return (int)fminf(floorf(dn), (float)n_rg); };
+
+    if constexpr (!S::ON) {
+        // each point reads its own eight rows
+        float4 rw[P];
+        static_for<0, P>([&](auto ic) { rw[ic] = rows[t + T * decltype(ic)::value]; });
+        __syncthreads();  // itab
+        static_for<0, P>([&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            const float dn = r0.x * rw[i].x;
+            const unsigned off = (unsigned)(n + shift(dn) - 3) * rb + (unsigned)((t + T * i) * EL);
+            v[i] = rcmc_point<K>(dn, r0, rw[i], itab,
+                                 [&](int j) { return Store<ST>::load(r, off + (unsigned)j * rb, 0u); });
+        });
+    } else {
+        float2 *stage = reinterpret_cast<float2 *>(lds);
+        auto fetch = [&](int i, float4 rwi, float2 (&z)[S::LOADS]) {
+            const unsigned off = (unsigned)(n0 + shift(r00 * rwi.x) - 3) * rb + (unsigned)((t + T * i) * EL);
+            static_for<0, S::LOADS>([&](auto uc) {
+                constexpr int u = decltype(uc)::value;
+                const int m = c + u * K::C;
+                z[u] = Store<ST>::load(r, off + (unsigned)m * rb, 0u);
+            });
+        };
+        auto put = [&](int buf, const float2 (&z)[S::LOADS]) {
+            static_for<0, S::LOADS>([&](auto uc) {
+                constexpr int u = decltype(uc)::value;
+                const int m = c + u * K::C;
+                stage[buf * (S::FLOATS / 2) + m * T + t] = z[u];
+            });
+        };
+        // row-table entries rotate through three registers: i (computed),
+        // i+1 (its rows in flight), i+2 (being read)
+        float4 rw0 = rows[t], rw1 = P > 1 ? rows[t + T] : rw0;
+        float2 z[S::LOADS];
+        fetch(0, rw0, z);
+        put(0, z);
+        __syncthreads();  // itab and the first chunk
+        static_for<0, P>([&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            float4 rw2 = rw1;
+            if constexpr (i + 2 < P) rw2 = rows[t + T * (i + 2)];
+            float2 zn[S::LOADS];
+            if constexpr (i + 1 < P) fetch(i + 1, rw1, zn);  // next chunk in flight
+            const float dn = r0.x * rw0.x;
+            // this point's rows sit c + (s - s0) rows into the window
+            const int d = min(shift(dn) - shift(r00 * rw0.x), 2);
+            const float2 *zs = stage + (i & 1) * (S::FLOATS / 2) + (c + d) * T + t;
+            v[i] = rcmc_point<K>(dn, r0, rw0, itab, [&](int j) { return zs[j * T]; });
+            if constexpr (i + 1 < P) put((i + 1) & 1, zn);
+            __syncthreads();  // chunk i+1 staged; chunk i's buffer free for i+2
+            rw0 = rw1;
+            rw1 = rw2;
+        });
+    }
+}
+
+// Store through LDS in the other thread-to-data map, for kernels whose input
+// and output run along different axes: a row-mapped kernel (consecutive
+// lanes hold consecutive points) writing strided columns hands each lane a
+// point of a neighbouring transform instead (C-element pieces of a row); a
+// column-mapped kernel writing contiguous rows hands consecutive lanes
+// consecutive points (whole rows).
+template <class K, int ST>
+__device__ __forceinline__ void store_remapped(float2 (&v)[K::P], void *__restrict__ out, long long blk, int c,
+                                               int t, const KArgs &a, float *lds) {
+    constexpr int P = K::P, T = K::T;
+    const int tid = threadIdx.x;
+    const int c2 = K::COLS ? (tid >> K::LOG_T) : (tid & (K::C - 1));
+    const int t2 = K::COLS ? (tid & (K::T - 1)) : (tid >> K::LOG_C);
+    const int wbase = lds_index<K>(t, c), rbase = lds_index<K>(t2, c2);
+    __syncthreads();  // the transform's last LDS reads are done
+    if constexpr (K::XCHG == XCHG_FULL) {
+        float2 *L = reinterpret_cast<float2 *>(lds);
+        static_for<0, P>([&](auto ic) { L[wbase + lds_offset<K>(T * decltype(ic)::value)] = v[ic]; });
+        __syncthreads();
+        static_for<0, P>([&](auto ic) { v[ic] = L[rbase + lds_offset<K>(T * decltype(ic)::value)]; });
+    } else {
+        static_for<0, P>([&](auto ic) { lds[wbase + lds_offset<K>(T * decltype(ic)::value)] = v[ic].x; });
+        __syncthreads();
+        float re[P];
+        static_for<0, P>([&](auto ic) { re[ic] = lds[rbase + lds_offset<K>(T * decltype(ic)::value)]; });
+        __syncthreads();
+        static_for<0, P>([&](auto ic) { lds[wbase + lds_offset<K>(T * decltype(ic)::value)] = v[ic].y; });
+        __syncthreads();
+        static_for<0, P>([&](auto ic) {
+            v[ic] = make_float2(re[ic], lds[rbase + lds_offset<K>(T * decltype(ic)::value)]);
+        });
+    }
+    if (blk * K::C + c2 < a.batch) store_points<K, ST, false>(v, out, blk, c2, t2, a);
 }
 
 // The whole on-chip computation of one transform (first exchange of the
@@ -386,6 +584,12 @@ __device__ __forceinline__ void transform(float2 (&v)[K::P], int t, int c, const
         });
         __builtin_amdgcn_sched_barrier(0);
         run_fft<K, !INV, false, false>(typename K::Rad{}, v, t, c, tw, lds, spec, h);
+    }
+    if constexpr (EPI == EPI_SCALE) {
+        static_for<0, K::P>([&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            v[i] = make_float2(v[i].x * scale, v[i].y * scale);
+        });
     }
 }
 
@@ -416,9 +620,19 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
     if constexpr (!K::PERSIST) {
         const long long blk = logical_block(a.xcd_remap);
         const bool valid = blk * K::C + c < a.batch;
-        load_points<K, IN_ST>(v, in, blk, c, t, valid, a);
-        transform<K, INV, EPI, true>(v, t, c, tw, spec, a.scale, lds);
-        if (valid) store_points<K, OUT_ST, NT>(v, out, blk, c, t, a);
+        if constexpr (EPI == EPI_RCMC) {
+            rcmc_load<K, IN_ST>(v, in, blk, c, t, valid, a, spec, lds);
+            transform<K, INV, EPI_NONE, true>(v, t, c, tw, spec, a.scale, lds);
+        } else {
+            load_points<K, IN_ST>(v, in, blk, c, t, valid, a);
+            transform<K, INV, EPI, true>(v, t, c, tw, spec, a.scale, lds);
+        }
+        if constexpr (EPI == EPI_RCMC || EPI == EPI_SCALE) {
+            // input and output run along different axes of the image
+            store_remapped<K, OUT_ST>(v, out, blk, c, t, a, lds);
+        } else {
+            if (valid) store_points<K, OUT_ST, NT>(v, out, blk, c, t, a);
+        }
     } else {
         // persistent: this workgroup takes blocks blockIdx.x, + gridDim.x, ...
         const long long nblk = (a.batch + K::C - 1) / K::C;

@@ -6,30 +6,69 @@
 
 namespace mi355fft {
 
-enum { LAYOUT_ROWS = 0, LAYOUT_COLS = 1 };
-enum { EPI_NONE = 0, EPI_MATCHED = 1 };
+// Kernel families: contiguous rows, strided column strips, and the
+// migration-correction pass (row-mapped kernels over the transposed
+// range-Doppler image that write columns of the focused image).
+enum { LAYOUT_ROWS = 0, LAYOUT_COLS = 1, LAYOUT_RCMC = 2 };
+// Per-kernel fusions around the transform:
+//   EPI_NONE     the plain transform;
+//   EPI_MATCHED  forward, X * conj(spec) * scale, inverse (range or azimuth
+//                compression in one pass);
+//   EPI_SCALE    forward, output * scale (the azimuth FFT with its 1/N_a),
+//                column strips in, written as rows (out_stride 1);
+//   EPI_RCMC     the load stage gathers, interpolates and phase-rotates the
+//                transposed range-Doppler image (migration correction and
+//                azimuth filter), the inverse transform runs, and the result
+//                is written as columns; `spec` points to the range-Doppler
+//                tables below.
+enum { EPI_NONE = 0, EPI_MATCHED = 1, EPI_SCALE = 2, EPI_RCMC = 3 };
+
+// Range-Doppler tables, one device block in this order (byte offsets from
+// rd_tables_layout; the interpolator rows are copied in from `interp_src`):
+//   rows   float4[n_az]  {(1/D_k - 1) / range_bin, 2 (D_k - 1) / lambda as a
+//                         hi + lo pair of floats, 0}
+//   cols   float2[n_rg]  {R0_n as a hi + lo pair}
+//   interp float2[(kRcmcSub + 1) * kRcmcTaps]  {g_q[j], g_{q+1}[j] - g_q[j]}
+constexpr int kRcmcSub = 128, kRcmcTaps = 8;
+struct RdTablesLayout {
+    long long rows, cols, interp, bytes;
+};
+__host__ __device__ constexpr long long round_up_256(long long x) { return (x + 255) & ~255LL; }
+__host__ __device__ constexpr RdTablesLayout rd_tables_layout(long long n_az, long long n_rg) {
+    return RdTablesLayout{0, round_up_256(n_az * 16), round_up_256(n_az * 16) + round_up_256(n_rg * 8),
+                          round_up_256(n_az * 16) + round_up_256(n_rg * 8) +
+                              round_up_256((long long)(kRcmcSub + 1) * kRcmcTaps * 8)};
+}
+
+// Fills the range-Doppler tables (double-precision arithmetic on the device,
+// rounded once to FP32 or split into FP32 hi + lo pairs).
+hipError_t launch_rd_tables(long long n_az, long long n_rg, double wavelength, double speed, double prf,
+                            double range_bin, double r_near, const float2 *interp_src, void *tables,
+                            hipStream_t s);
 
 struct KArgs {
-    long long batch;     // transforms
-    long long stride;    // elements between points of a transform (input and output)
-    long long in_dist;   // elements between transform starts in the input
-    long long out_dist;  // elements between transform starts in the output
-    float scale;         // epilogue scale
-    int xcd_remap;       // 1: map blocks so consecutive strips share an XCD
-    int wide;            // 1: 64-bit pointer addressing (span or sign does not fit buffer offsets)
-    unsigned in_span;    // bytes one workgroup's input occupies (buffer addressing)
-    unsigned out_span;   // bytes one workgroup's output occupies
+    long long batch;       // transforms
+    long long stride;      // elements between points of a transform in the input
+    long long in_dist;     // elements between transform starts in the input
+    long long out_dist;    // elements between transform starts in the output
+    float scale;           // epilogue scale
+    int xcd_remap;         // 1: map blocks so consecutive strips share an XCD
+    int wide;              // 1: 64-bit pointer addressing (span or sign does not fit buffer offsets)
+    unsigned in_span;      // bytes one workgroup's input occupies (buffer addressing)
+    unsigned out_span;     // bytes one workgroup's output occupies
+    long long out_stride;  // elements between points of a transform in the output; 0: same as the input
 };
 
 // Fills the addressing fields of `a` for workgroups of `c` transforms of `n`
 // points with elements of in_bytes / out_bytes.
 inline void set_spans(KArgs &a, long long n, long long c, int in_bytes, int out_bytes) {
     const long long lim = 0x7fffffffLL;
+    if (a.out_stride == 0) a.out_stride = a.stride;
     const long long cc = c < a.batch ? c : a.batch;
     const long long in_el = (cc - 1) * a.in_dist + (n - 1) * a.stride + 1;
-    const long long out_el = (cc - 1) * a.out_dist + (n - 1) * a.stride + 1;
-    const bool ok = a.in_dist >= 0 && a.out_dist >= 0 && a.stride >= 1 && in_el * in_bytes <= lim &&
-                    out_el * out_bytes <= lim;
+    const long long out_el = (cc - 1) * a.out_dist + (n - 1) * a.out_stride + 1;
+    const bool ok = a.in_dist >= 0 && a.out_dist >= 0 && a.stride >= 1 && a.out_stride >= 1 &&
+                    in_el * in_bytes <= lim && out_el * out_bytes <= lim;
     a.wide = ok ? 0 : 1;
     a.in_span = ok ? (unsigned)(in_el * in_bytes) : 0u;
     a.out_span = ok ? (unsigned)(out_el * out_bytes) : 0u;

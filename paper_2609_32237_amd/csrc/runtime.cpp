@@ -76,6 +76,73 @@ int get_twiddles(int device, int64_t n, const float2 **out) {
     return FFT_OK;
 }
 
+// The migration-correction interpolator (Section X): an 8-tap sinc under a
+// Kaiser window (beta 2.5) spanning the 8 taps, at the 129 fractional shifts
+// mu = q / 128, each row normalised to unit sum, stored as FP32 pairs
+// {g_q[j], g_{q+1}[j] - g_q[j]} for linear blending between rows (Section X's
+// third fix).  Tap j sits at offset j - 3 from the integer part of the
+// position.  Computed in double once per device.
+std::mutex g_interp_mutex;
+std::map<int, float2 *> g_interp;
+
+double bessel_i0(double x) {  // sum_m ((x/2)^m / m!)^2
+    double term = 1.0, sum = 1.0;
+    const double h = 0.25 * x * x;
+    for (int m = 1; m < 200 && term >= 1e-18 * sum; ++m) {
+        term *= h / ((double)m * (double)m);
+        sum += term;
+    }
+    return sum;
+}
+
+void interp_row(int q, double *g) {
+    using mi355fft::kRcmcSub;
+    using mi355fft::kRcmcTaps;
+    const double pi = 3.141592653589793238462643383279, beta = 2.5;
+    const double mu = (double)q / kRcmcSub, inv_i0 = 1.0 / bessel_i0(beta);
+    double sum = 0.0;
+    for (int j = 0; j < kRcmcTaps; ++j) {
+        const double x = (double)(j - 3) - mu;
+        const double sinc = x == 0.0 ? 1.0 : std::sin(pi * x) / (pi * x);
+        const double r = 0.25 * x, arg = 1.0 - r * r;
+        g[j] = sinc * bessel_i0(beta * std::sqrt(arg > 0.0 ? arg : 0.0)) * inv_i0;
+        sum += g[j];
+    }
+    for (int j = 0; j < kRcmcTaps; ++j) g[j] /= sum;
+}
+
+int get_interp(int device, const float2 **out) {
+    using mi355fft::kRcmcSub;
+    using mi355fft::kRcmcTaps;
+    std::lock_guard<std::mutex> lock(g_interp_mutex);
+    auto it = g_interp.find(device);
+    if (it != g_interp.end()) {
+        *out = it->second;
+        return FFT_OK;
+    }
+    std::vector<float2> host((size_t)(kRcmcSub + 1) * kRcmcTaps);
+    double g[kRcmcTaps], g1[kRcmcTaps];
+    for (int q = 0; q <= kRcmcSub; ++q) {
+        interp_row(q, g);
+        if (q < kRcmcSub) interp_row(q + 1, g1);
+        for (int j = 0; j < kRcmcTaps; ++j) {
+            const float lo = (float)g[j];
+            host[(size_t)(q * kRcmcTaps + j)] = make_float2(lo, q < kRcmcSub ? (float)(g1[j] - (double)lo) : 0.0f);
+        }
+    }
+    float2 *dev = nullptr;
+    hipError_t e = hipMalloc((void **)&dev, sizeof(float2) * host.size());
+    if (e != hipSuccess) return map_hip(e);
+    e = hipMemcpy(dev, host.data(), sizeof(float2) * host.size(), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        (void)hipFree(dev);
+        return map_hip(e);
+    }
+    g_interp[device] = dev;
+    *out = dev;
+    return FFT_OK;
+}
+
 hipError_t launch_fft(int64_t n, int variant, int layout, int in_st, int out_st, int inv, int epi, const void *in,
                       void *out, const float2 *tw, const float2 *spec, const KArgs &a, hipStream_t s) {
     using namespace mi355fft;
@@ -102,10 +169,13 @@ int variant_count(int64_t n, int layout) {
 }
 
 // Kernel-shape override for tests and tuning: MI355FFT_ROW_VARIANT /
-// MI355FFT_COL_VARIANT = index into the size's variant list (unset: default).
+// MI355FFT_COL_VARIANT / MI355FFT_RCMC_VARIANT = index into the size's list of
+// row, column or migration-correction kernels (unset: default).
 // Returns -1 for the default, -2 for an index the size does not have.
 int chosen_variant(int64_t n, int layout) {
-    const char *e = std::getenv(layout == mi355fft::LAYOUT_ROWS ? "MI355FFT_ROW_VARIANT" : "MI355FFT_COL_VARIANT");
+    const char *e = std::getenv(layout == mi355fft::LAYOUT_ROWS   ? "MI355FFT_ROW_VARIANT"
+                                : layout == mi355fft::LAYOUT_COLS ? "MI355FFT_COL_VARIANT"
+                                                                  : "MI355FFT_RCMC_VARIANT");
     if (!e || !e[0]) return -1;
     char *end = nullptr;
     long v = std::strtol(e, &end, 10);
@@ -114,6 +184,23 @@ int chosen_variant(int64_t n, int layout) {
 }
 
 bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+bool overlaps(const void *a, size_t na, const void *b, size_t nb) {
+    const char *pa = (const char *)a, *pb = (const char *)b;
+    return pa < pb + nb && pb < pa + na;
+}
+
+// Full range-Doppler chain: the migration-correction pass addresses the whole
+// intermediate image through one 31-bit buffer offset, so n_az * n_rg * 8
+// bytes must stay below 2 GiB.
+constexpr int64_t kMaxRdPoints = int64_t(1) << 27;
+constexpr double kMaxDopplerRatio = 1.0 / 3.0;  // 15 (1 / sqrt(1 - 1/9) - 1) = 0.91
+
+// Workspace of sar_rd_form_image: range reference spectrum, tables, image.
+size_t rd_tables_offset(int64_t n_rg) { return (size_t)n_rg * sizeof(float2); }  // n_rg >= 1024: 256-aligned
+size_t rd_mid_offset(int64_t n_az, int64_t n_rg) {
+    return rd_tables_offset(n_rg) + (size_t)mi355fft::rd_tables_layout(n_az, n_rg).bytes;
+}
 
 // The library-owned workspace of the fixed-size sar_form_image, per device.
 std::mutex g_ws_mutex;
@@ -201,11 +288,7 @@ int sar_form_image_ex(int64_t n_az, int64_t n_rg, int inter_storage, const void 
         return FFT_EALIGN;
     const size_t img = (size_t)n_az * (size_t)n_rg * 8;
     const size_t ws = sar_workspace_bytes(n_az, n_rg, inter_storage);
-    auto overlap = [](const void *a, size_t na, const void *b, size_t nb) {
-        const char *pa = (const char *)a, *pb = (const char *)b;
-        return pa < pb + nb && pb < pa + na;
-    };
-    if (overlap(out, img, raw, img) || overlap(out, img, workspace, ws) || overlap(raw, img, workspace, ws))
+    if (overlaps(out, img, raw, img) || overlaps(out, img, workspace, ws) || overlaps(raw, img, workspace, ws))
         return FFT_EINVAL;
 
     int device = 0;
@@ -256,6 +339,85 @@ int sar_form_image_ex(int64_t n_az, int64_t n_rg, int inter_storage, const void 
     const KArgs ac{n_rg, n_rg, 1, 1, (float)(1.0 / (double)n_az), 1};
     e = launch_fft(n_az, vcol, LAYOUT_COLS, inter_storage, FFT_STORAGE_FP32, 0, EPI_MATCHED, mid, out, tw_az, h_az,
                    ac, stream);
+    return map_hip(e);
+}
+
+size_t sar_rd_workspace_bytes(int64_t n_az, int64_t n_rg, int inter_storage) {
+    if (!supported_n(n_az) || !supported_n(n_rg) || n_az * n_rg > kMaxRdPoints) return 0;
+    if (inter_storage != FFT_STORAGE_FP32 && inter_storage != FFT_STORAGE_FP16) return 0;
+    const size_t el = inter_storage == FFT_STORAGE_FP32 ? 8 : 4;
+    return rd_mid_offset(n_az, n_rg) + (size_t)n_az * (size_t)n_rg * el;
+}
+
+int sar_rd_form_image(int64_t n_az, int64_t n_rg, int inter_storage, const sar_geometry *geo, const void *raw,
+                      const void *range_ref, void *out, void *workspace, hipStream_t stream) {
+    if (!geo || !raw || !range_ref || !out || !workspace) return FFT_EINVAL;
+    if (inter_storage != FFT_STORAGE_FP32 && inter_storage != FFT_STORAGE_FP16) return FFT_EINVAL;
+    if (n_az < 1 || n_rg < 1) return FFT_EINVAL;
+    const double g[5] = {geo->wavelength, geo->speed, geo->prf, geo->range_bin, geo->r_near};
+    for (double x : g)
+        if (!(x > 0.0) || !std::isfinite(x)) return FFT_EINVAL;
+    const double x_max = geo->wavelength * geo->prf / (4.0 * geo->speed);  // lambda f_a / 2v at prf / 2
+    if (!(x_max < 1.0)) return FFT_EINVAL;
+    if (!supported_n(n_az) || !supported_n(n_rg) || n_az * n_rg > kMaxRdPoints) return FFT_EUNSUPPORTED;
+    // the migration-correction pass shares one window of rows across a strip
+    // of up to 16 range bins, which needs the shift to change by less than a
+    // bin across the strip: 15 (1/D - 1) < 1 at the band edge
+    if (x_max > kMaxDopplerRatio) return FFT_EUNSUPPORTED;
+    if (!aligned(raw, 8) || !aligned(range_ref, 8) || !aligned(out, 8) || !aligned(workspace, 256))
+        return FFT_EALIGN;
+    const size_t img = (size_t)n_az * (size_t)n_rg * 8;
+    const size_t ws = sar_rd_workspace_bytes(n_az, n_rg, inter_storage);
+    if (overlaps(out, img, raw, img) || overlaps(out, img, workspace, ws) || overlaps(raw, img, workspace, ws))
+        return FFT_EINVAL;
+
+    int device = 0;
+    hipError_t e = hipGetDevice(&device);
+    if (e != hipSuccess) return map_hip(e);
+    const float2 *tw_rg = nullptr, *tw_az = nullptr;
+    int rc = get_twiddles(device, n_rg, &tw_rg);
+    if (rc == FFT_OK) rc = get_twiddles(device, n_az, &tw_az);
+    if (rc != FFT_OK) return rc;
+    const int vrow = chosen_variant(n_rg, mi355fft::LAYOUT_ROWS);
+    const int vcol = chosen_variant(n_az, mi355fft::LAYOUT_COLS);
+    const int vrcmc = chosen_variant(n_az, mi355fft::LAYOUT_RCMC);
+    if (vrow == -2 || vcol == -2 || vrcmc == -2) return FFT_EINVAL;
+
+    const float2 *interp = nullptr;
+    rc = get_interp(device, &interp);
+    if (rc != FFT_OK) return rc;
+
+    using namespace mi355fft;
+    char *wsb = reinterpret_cast<char *>(workspace);
+    float2 *h_rg = reinterpret_cast<float2 *>(wsb);
+    void *tables = wsb + rd_tables_offset(n_rg);
+    void *zt = wsb + rd_mid_offset(n_az, n_rg);
+
+    e = launch_rd_tables(n_az, n_rg, g[0], g[1], g[2], g[3], g[4], interp, tables, stream);
+    if (e != hipSuccess) return map_hip(e);
+    const KArgs aref{1, 1, n_rg, n_rg, 1.0f, 0};
+    e = launch_fft(n_rg, vrow, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, range_ref, h_rg, tw_rg, nullptr, aref, stream);
+    if (e != hipSuccess) return map_hip(e);
+    // 1: range compression, rows: FFT, * conj(H_r) / n_rg, IFFT.  The
+    //    range-compressed image is kept in `out`, which the last pass
+    //    overwrites with the focused image.
+    const KArgs ar{n_az, 1, n_rg, n_rg, (float)(1.0 / (double)n_rg), 0};
+    e = launch_fft(n_rg, vrow, LAYOUT_ROWS, FFT_STORAGE_FP32, inter_storage, 0, EPI_MATCHED, raw, out, tw_rg, h_rg,
+                   ar, stream);
+    if (e != hipSuccess) return map_hip(e);
+    // 2: azimuth FFT of every range bin (a column), / n_az, written as one row
+    //    per range bin (the transposed range-Doppler image)
+    KArgs ab{n_rg, n_rg, 1, n_az, (float)(1.0 / (double)n_az), 1};
+    ab.out_stride = 1;
+    e = launch_fft(n_az, vcol, LAYOUT_COLS, inter_storage, inter_storage, 0, EPI_SCALE, out, zt, tw_az, nullptr, ab,
+                   stream);
+    if (e != hipSuccess) return map_hip(e);
+    // 3-5: migration correction, azimuth filter and azimuth inverse FFT: reads
+    //    rows of the transposed image, writes the columns of the focused image
+    KArgs ac{n_rg, 1, n_az, 1, 1.0f, 1};
+    ac.out_stride = n_rg;
+    e = launch_fft(n_az, vrcmc, LAYOUT_RCMC, inter_storage, FFT_STORAGE_FP32, 1, EPI_RCMC, zt, out, tw_az,
+                   reinterpret_cast<const float2 *>(tables), ac, stream);
     return map_hip(e);
 }
 

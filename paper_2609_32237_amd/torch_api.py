@@ -90,3 +90,24 @@ def sar_form_image(raw: torch.Tensor, range_ref: torch.Tensor, az_ref: torch.Ten
     _lib.sar_form_image_ex(n_az, n_rg, inter_storage, raw.data_ptr(), range_ref.data_ptr(),
                            az_ref.data_ptr(), out.data_ptr(), workspace.data_ptr(), _stream(stream))
     return out
+
+
+def sar_rd_form_image(raw: torch.Tensor, range_ref: torch.Tensor, geometry,
+                      inter_storage: int = FFT_STORAGE_FP32, out: torch.Tensor | None = None,
+                      workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Focused image of a (n_az, n_rg) complex64 stripmap echo by the full
+    range-Doppler chain; ``geometry`` maps wavelength, speed, prf, range_bin
+    and r_near to their values."""
+    n_az, n_rg = raw.shape
+    for t in (raw, range_ref):
+        if t.dtype != torch.complex64 or not t.is_cuda or not t.is_contiguous():
+            raise TypeError("raw and range_ref must be contiguous complex64 GPU tensors")
+    out = torch.empty_like(raw) if out is None else out
+    nbytes = _lib.sar_rd_workspace_bytes(n_az, n_rg, inter_storage)
+    if nbytes == 0:
+        raise _lib.FFTError(_lib.FFT_EUNSUPPORTED, "sar_rd_workspace_bytes")
+    if workspace is None:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=raw.device)
+    _lib.sar_rd_form_image(n_az, n_rg, inter_storage, geometry, raw.data_ptr(), range_ref.data_ptr(),
+                           out.data_ptr(), workspace.data_ptr(), _stream(stream))
+    return out

@@ -31,7 +31,7 @@ def declared_functions():
 def test_header_declares_the_abi():
     assert declared_functions() == sorted(
         ["fft_plan_create", "fft_execute", "fft_plan_destroy", "sar_workspace_bytes", "sar_form_image_ex",
-         "sar_form_image", "fft_strerror"])
+         "sar_form_image", "sar_rd_workspace_bytes", "sar_rd_form_image", "fft_strerror"])
 
 
 def test_library_exports_every_declared_symbol(L):
@@ -145,3 +145,40 @@ def test_out_of_range_variant_is_rejected_before_any_hip_call(var, value):
                          timeout=120)
     assert res.returncode == 0, res.stderr
     assert int(res.stdout.split()[0]) == -1
+
+
+def test_sar_rd_workspace_bytes(L):
+    def up(x):
+        return (x + 255) // 256 * 256
+    tables = up(4096 * 16) + up(4096 * 8) + up(129 * 8 * 8)
+    assert L.sar_rd_workspace_bytes(4096, 4096, 0) == 4096 * 8 + tables + 4096 * 4096 * 8
+    assert L.sar_rd_workspace_bytes(4096, 4096, 1) == 4096 * 8 + tables + 4096 * 4096 * 4
+    assert L.sar_rd_workspace_bytes(16384, 8192, 0) == 8192 * 8 + up(16384 * 16) + up(8192 * 8) + up(129 * 64) + \
+        16384 * 8192 * 8
+    assert L.sar_rd_workspace_bytes(16384, 16384, 0) == 0  # beyond 2^27 points
+    assert L.sar_rd_workspace_bytes(4096, 4000, 0) == 0
+    assert L.sar_rd_workspace_bytes(4096, 4096, 2) == 0
+
+
+def test_sar_rd_argument_errors(L):
+    f = L.lib.sar_rd_form_image
+    geo = L.geometry(dict(wavelength=0.24, speed=200.0, prf=500.0, range_bin=1.249, r_near=17500.0))
+    g = ctypes.byref(geo)
+    ok = 1 << 20
+    ws = 1 << 40
+    assert f(4096, 4096, 0, None, ok, ok, 1 << 36, ws, None) == L.FFT_EINVAL        # no geometry
+    assert f(4096, 4096, 0, g, None, ok, 1 << 36, ws, None) == L.FFT_EINVAL         # no echo
+    assert f(4096, 4096, 2, g, ok, ok, 1 << 36, ws, None) == L.FFT_EINVAL           # bad storage
+    for field, bad in (("wavelength", 0.0), ("speed", -1.0), ("prf", float("nan")), ("range_bin", float("inf")),
+                       ("r_near", 0.0), ("prf", 3400.0)):  # prf 3400: lambda prf / 4v >= 1
+        b = L.geometry(dict(wavelength=0.24, speed=200.0, prf=500.0, range_bin=1.249, r_near=17500.0))
+        setattr(b, field, bad)
+        assert f(4096, 4096, 0, ctypes.byref(b), ok, ok, 1 << 36, ws, None) == L.FFT_EINVAL, field
+    wide_band = L.geometry(dict(wavelength=0.24, speed=200.0, prf=1400.0, range_bin=1.249, r_near=17500.0))
+    assert f(4096, 4096, 0, ctypes.byref(wide_band), ok, ok, 1 << 36, ws, None) == L.FFT_EUNSUPPORTED  # 0.42 > 1/3
+    assert f(4000, 4096, 0, g, ok, ok, 1 << 36, ws, None) == L.FFT_EUNSUPPORTED
+    assert f(16384, 16384, 0, g, ok, ok, 1 << 36, ws, None) == L.FFT_EUNSUPPORTED   # beyond 2^27 points
+    assert f(4096, 4096, 0, g, ok + 4, ok, 1 << 36, ws, None) == L.FFT_EALIGN
+    assert f(4096, 4096, 0, g, ok, ok, 1 << 36, ws + 8, None) == L.FFT_EALIGN       # workspace 256 B
+    assert f(4096, 4096, 0, g, 1 << 30, ok, (1 << 30) + 4096, ws, None) == L.FFT_EINVAL  # out overlaps raw
+    assert f(4096, 4096, 0, g, ok, ok, ws + 4096, ws, None) == L.FFT_EINVAL         # out inside workspace
