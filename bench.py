@@ -14,8 +14,10 @@ time of the K timed steps.  The JSON line also carries:
   cpu_baseline  the fp64 oracle timed on this host on a bounded sample of the
                 same workload;
   breakdown     the other workloads (N = 1024 latency case, 8192, 16384, FP16
-                storage, and the 4096 x 4096 SAR image with FP32 and FP16
-                intermediates), each a median of cache-flushed samples.
+                storage, the 4096 x 4096 two-pass SAR image and the 4096 x
+                4096 full range-Doppler image of the paper's L-band scene, with
+                FP32 and FP16 intermediates), each a median of cache-flushed
+                samples.
 """
 from __future__ import annotations
 
@@ -122,6 +124,26 @@ def sar_breakdown(torch, api, flush, inter, samples):
     bytes_ = bpp * 4096 * 4096
     gbs = bytes_ / (med * 1e-3) / 1e9
     return {"image": "4096x4096", "intermediate": "fp32" if inter == 0 else "fp16", "ms_median": round(med, 5),
+            "ms_iqr": [round(q1, 5), round(q3, 5)], "algorithmic_bytes_per_point": bpp, "GB/s": round(gbs, 1),
+            "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)}
+
+
+def rd_breakdown(torch, api, flush, inter, samples):
+    """The paper's full range-Doppler chain on its 4096 x 4096 L-band scene."""
+    import workloads
+
+    sc = workloads.rd_scene()
+    raw = torch.from_numpy(sc.raw).cuda()
+    hr = torch.from_numpy(sc.range_ref).cuda()
+    out = torch.empty_like(raw)
+    ws = torch.empty(api._lib.sar_rd_workspace_bytes(4096, 4096, inter), dtype=torch.uint8, device="cuda")
+    fn = lambda: api.sar_rd_form_image(raw, hr, sc.geometry, inter, out=out, workspace=ws)  # noqa: E731
+    med, q1, q3 = time_samples(torch, fn, flush, samples)
+    # raw read, range-compressed write + read, range-Doppler write + read, image write
+    bpp = 48 if inter == 0 else 32
+    gbs = bpp * 4096 * 4096 / (med * 1e-3) / 1e9
+    return {"image": "4096x4096", "scene": "L-band stripmap, 6 targets (Section X)",
+            "intermediate": "fp32" if inter == 0 else "fp16", "passes": 3, "ms_median": round(med, 5),
             "ms_iqr": [round(q1, 5), round(q3, 5)], "algorithmic_bytes_per_point": bpp, "GB/s": round(gbs, 1),
             "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)}
 
@@ -335,6 +357,10 @@ def main():
         for inter in (0, 1):
             log(f"breakdown sar inter={inter}")
             bd[f"sar_4096x4096_{'fp32' if inter == 0 else 'fp16'}_inter"] = sar_breakdown(
+                torch, api, flush, inter, args.samples)
+        for inter in (0, 1):
+            log(f"breakdown range-Doppler inter={inter}")
+            bd[f"rd_4096x4096_{'fp32' if inter == 0 else 'fp16'}_inter"] = rd_breakdown(
                 torch, api, flush, inter, args.samples)
         result["breakdown"] = bd
     print(json.dumps(result), flush=True)

@@ -397,9 +397,10 @@ __device__ __forceinline__ void store_points(const float2 (&v)[K::P], void *__re
 // thread's own k for each i): the workgroup stages the chunk's W >= C + 10
 // rows into LDS (each thread loads W / C of them for its k, one row per load
 // instruction of the wave: contiguous pieces), then each thread reads its
-// eight taps from there.  Two staging buffers alternate, so one barrier per
-// chunk separates writing a buffer from reading it, and the next chunk's
-// loads are in flight while the current one is computed.
+// eight taps from there.  G chunks share a barrier and two buffers of them
+// alternate, so one barrier per G chunks separates writing a buffer from
+// reading it, and the next G chunks' loads are in flight while the current
+// ones are computed.
 // The image is addressed through one buffer resource spanning its n_rg rows
 // (the host guarantees it fits 31 bits), each row with its own 32-bit offset:
 // rows outside [0, n_rg) fall outside the resource (a negative row wraps to an
@@ -411,9 +412,13 @@ struct RcmcStage {
     // under a lane condition costs the compiler far more than the row)
     static constexpr int LOADS = (K::C + 10 + K::C - 1) / K::C;  // rows each thread loads
     static constexpr int W = LOADS * K::C;                        // staged rows per Doppler bin
-    static constexpr int FLOATS = 2 * W * K::T;                   // one buffer, complex
+    static constexpr int FLOATS = 2 * W * K::T;                   // one chunk, complex
     // staging pays when the strip shares taps (C >= 4) and two buffers fit
     static constexpr bool ON = K::C >= 4 && 2 * FLOATS <= K::LDS_FLOATS;
+    // chunks staged per barrier: as many as two buffers of them fit (1, 2 or 4)
+    static constexpr int G = (K::P % 4 == 0 && 8 * FLOATS <= K::LDS_FLOATS)   ? 4
+                             : (K::P % 2 == 0 && 4 * FLOATS <= K::LDS_FLOATS) ? 2
+                                                                             : 1;
 };
 
 // Point i of thread (t, c): interpolation of the taps z(j) = Z[n + s - 3 + j]
@@ -488,43 +493,62 @@ __device__ __forceinline__ void rcmc_load(float2 (&v)[K::P], const void *__restr
         });
     } else {
         float2 *stage = reinterpret_cast<float2 *>(lds);
+        constexpr int G = S::G, HALF = G * (S::FLOATS / 2);  // float2 per buffer
         auto fetch = [&](int i, float4 rwi, float2 (&z)[S::LOADS]) {
             const unsigned off = (unsigned)(n0 + shift(r00 * rwi.x) - 3) * rb + (unsigned)((t + T * i) * EL);
             static_for<0, S::LOADS>([&](auto uc) {
                 constexpr int u = decltype(uc)::value;
-                const int m = c + u * K::C;
-                z[u] = Store<ST>::load(r, off + (unsigned)m * rb, 0u);
+                z[u] = Store<ST>::load(r, off + (unsigned)(c + u * K::C) * rb, 0u);
             });
         };
-        auto put = [&](int buf, const float2 (&z)[S::LOADS]) {
+        // chunk i lives in buffer (i / G) & 1, slot i % G
+        auto put = [&](int i, const float2 (&z)[S::LOADS]) {
+            float2 *dst = stage + ((i / G) & 1) * HALF + (i % G) * (S::FLOATS / 2) + t;
             static_for<0, S::LOADS>([&](auto uc) {
                 constexpr int u = decltype(uc)::value;
-                const int m = c + u * K::C;
-                stage[buf * (S::FLOATS / 2) + m * T + t] = z[u];
+                dst[(c + u * K::C) * T] = z[u];
             });
         };
-        // row-table entries rotate through three registers: i (computed),
-        // i+1 (its rows in flight), i+2 (being read)
-        float4 rw0 = rows[t], rw1 = P > 1 ? rows[t + T] : rw0;
-        float2 z[S::LOADS];
-        fetch(0, rw0, z);
-        put(0, z);
-        __syncthreads();  // itab and the first chunk
-        static_for<0, P>([&](auto ic) {
-            constexpr int i = decltype(ic)::value;
-            float4 rw2 = rw1;
-            if constexpr (i + 2 < P) rw2 = rows[t + T * (i + 2)];
-            float2 zn[S::LOADS];
-            if constexpr (i + 1 < P) fetch(i + 1, rw1, zn);  // next chunk in flight
-            const float dn = r0.x * rw0.x;
-            // this point's rows sit c + (s - s0) rows into the window
-            const int d = min(shift(dn) - shift(r00 * rw0.x), 2);
-            const float2 *zs = stage + (i & 1) * (S::FLOATS / 2) + (c + d) * T + t;
-            v[i] = rcmc_point<K>(dn, r0, rw0, itab, [&](int j) { return zs[j * T]; });
-            if constexpr (i + 1 < P) put((i + 1) & 1, zn);
-            __syncthreads();  // chunk i+1 staged; chunk i's buffer free for i+2
-            rw0 = rw1;
-            rw1 = rw2;
+        // row-table entries rotate through three register sets of G: chunks
+        // being computed, chunks whose rows are in flight, chunks being read
+        float4 rwc[G], rwn[G];
+        static_for<0, G>([&](auto gc) {
+            rwc[gc] = rows[t + T * decltype(gc)::value];
+            rwn[gc] = P / G > 1 ? rows[t + T * (G + decltype(gc)::value)] : rwc[gc];
+        });
+        static_for<0, G>([&](auto gc) {
+            float2 z[S::LOADS];
+            fetch(gc, rwc[gc], z);
+            put(gc, z);
+        });
+        __syncthreads();  // itab and the first G chunks
+        static_for<0, P / G>([&](auto bc) {
+            constexpr int b = decltype(bc)::value;
+            float4 rwf[G];
+            static_for<0, G>([&](auto gc) {
+                rwf[gc] = rwn[gc];
+                if constexpr (b + 2 < P / G) rwf[gc] = rows[t + T * ((b + 2) * G + decltype(gc)::value)];
+            });
+            float2 zn[G][S::LOADS];
+            if constexpr (b + 1 < P / G) {
+                static_for<0, G>([&](auto gc) { fetch((b + 1) * G + gc, rwn[gc], zn[gc]); });
+            }
+            static_for<0, G>([&](auto gc) {
+                constexpr int i = b * G + gc;
+                const float dn = r0.x * rwc[gc].x;
+                // this point's rows sit c + (s - s0) rows into the window
+                const int d = min(shift(dn) - shift(r00 * rwc[gc].x), 2);
+                const float2 *zs = stage + ((i / G) & 1) * HALF + (i % G) * (S::FLOATS / 2) + (c + d) * T + t;
+                v[i] = rcmc_point<K>(dn, r0, rwc[gc], itab, [&](int j) { return zs[j * T]; });
+            });
+            if constexpr (b + 1 < P / G) {
+                static_for<0, G>([&](auto gc) { put((b + 1) * G + gc, zn[gc]); });
+            }
+            __syncthreads();  // the next G chunks staged; these G chunks' buffer free
+            static_for<0, G>([&](auto gc) {
+                rwc[gc] = rwn[gc];
+                rwn[gc] = rwf[gc];
+            });
         });
     }
 }
