@@ -14,7 +14,7 @@ time of the K timed steps.  The JSON line also carries:
   cpu_baseline  the fp64 oracle timed on this host on a bounded sample of the
                 same workload;
   breakdown     the other workloads (N = 1024 latency case, 8192, 16384, FP16
-                storage, the 4096 x 4096 two-pass SAR image and the 4096 x
+                storage, a 2^20-point transform in the two-pass four-step form, the 4096 x 4096 two-pass SAR image and the 4096 x
                 4096 full range-Doppler image of the paper's L-band scene, with
                 FP32 and FP16 intermediates), each a median of cache-flushed
                 samples.
@@ -107,6 +107,22 @@ def fft_breakdown(torch, api, flush, name, samples):
     return {"n": n, "batch": batch, "storage": storage, "ms_median": round(med, 5), "ms_iqr": [round(q1, 5), round(q3, 5)],
             "GB/s": round(gbs, 1), "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
             "GFLOPS": round(gflops(n, batch, med * 1e-3), 1)}
+
+
+def long_breakdown(torch, api, flush, n, batch, samples):
+    """A transform longer than the chip holds: the two-pass four-step form.
+    GB/s counts the method's own 16 bytes per point (one read, one write);
+    the two passes move twice that."""
+    g = torch.Generator(device="cuda").manual_seed(11)
+    x = torch.view_as_complex(torch.rand(batch, n, 2, device="cuda", generator=g) * 2 - 1)
+    out = torch.empty_like(x)
+    plan = api.Plan(n, batch, 1, n, 0, -1)
+    med, q1, q3 = time_samples(torch, lambda: plan.execute(x, out), flush, samples)
+    plan.close()
+    gbs = 16 * n * batch / (med * 1e-3) / 1e9
+    return {"n": n, "batch": batch, "storage": "fp32", "passes": 2, "ms_median": round(med, 5),
+            "ms_iqr": [round(q1, 5), round(q3, 5)], "GB/s": round(gbs, 1), "moved_GB/s": round(2 * gbs, 1),
+            "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4), "GFLOPS": round(gflops(n, batch, med * 1e-3), 1)}
 
 
 def sar_breakdown(torch, api, flush, inter, samples):
@@ -354,6 +370,8 @@ def main():
                      "fft_n16384_b8192_fp32", "fft_n16384_b16384_fp16"):
             log(f"breakdown {name}")
             bd[name] = fft_breakdown(torch, api, flush, name, args.samples)
+        log("breakdown fft_n1048576_b128_fp32 (four-step)")
+        bd["fft_n1048576_b128_fp32"] = long_breakdown(torch, api, flush, 1 << 20, 128, args.samples)
         for inter in (0, 1):
             log(f"breakdown sar inter={inter}")
             bd[f"sar_4096x4096_{'fp32' if inter == 0 else 'fp16'}_inter"] = sar_breakdown(

@@ -68,8 +68,17 @@ typedef struct fft_plan fft_plan; /* opaque; immutable once created */
  * batch's footprint is its input plus its output); Section VII adds FP16
  * storage.
  *
- *   n        transform length: a power of two in [1024, 16384], else
- *            FFT_EUNSUPPORTED.
+ *   n        transform length: a power of two in [1024, 2^28], else
+ *            FFT_EUNSUPPORTED.  Up to 16384 every transform is one pass
+ *            (read once, written once).  Longer transforms use the two-pass
+ *            four-step form (Section VI: the transform no longer fits on
+ *            chip): n = n1 * n2 with n2 = 2^floor(log2(n) / 2); they require
+ *            stride == 1 (else FFT_EUNSUPPORTED) and out-of-place execution,
+ *            and use `out` for the intermediate.  Batches of at most 16
+ *            contiguous 16384-point transforms executed out of place take the
+ *            same split (128 x 128) to spread each transform over more
+ *            workgroups (Section VI's advice for small batches); in place
+ *            they stay single-pass.
  *   batch    number of transforms, >= 1.
  *   stride   distance between consecutive points of one transform, >= 1.
  *   dist     distance between the first points of consecutive transforms, >= 1.
@@ -87,8 +96,11 @@ typedef struct fft_plan fft_plan; /* opaque; immutable once created */
  *
  * Creates (once per device and size, shared by all plans, kept until the
  * process ends) a device table of the n twiddle factors exp(-2 pi i m / n),
- * computed in double precision on the host and rounded once to FP32.  Uses
- * the current HIP device; the plan must be executed on that device.
+ * computed in double precision on the host and rounded once to FP32; for
+ * four-step lengths, the tables of n1 and n2 and a two-level table of the
+ * factors exp(-2 pi i m / n) (about 2 sqrt(n) entries, W^m formed as the
+ * product of two entries).  Uses the current HIP device; the plan must be
+ * executed on that device.
  * Returns FFT_OK, FFT_EINVAL, FFT_EUNSUPPORTED, FFT_ENOMEM or FFT_EHIP.
  */
 int fft_plan_create(int64_t n, int64_t batch, int64_t stride, int64_t dist, int storage, int dir,
@@ -100,7 +112,8 @@ int fft_plan_create(int64_t n, int64_t batch, int64_t stride, int64_t dist, int 
  * Every transform is read from `in` once and written to `out` once (Section
  * VI: the whole transform stays on chip between its stages).
  *   in, out  device buffers laid out as the plan says; in == out (in place) is
- *            allowed, partial overlap is not.  Aligned to one complex element
+ *            allowed for n <= 16384 (FFT_EINVAL for longer transforms),
+ *            partial overlap is not.  Aligned to one complex element
  *            (8 bytes FP32, 4 bytes FP16), else FFT_EALIGN.
  *   stream   HIP stream the kernel is launched on.
  * Safe to call concurrently on different streams with the same plan.

@@ -637,6 +637,10 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
     // range-compression pass writes the intermediate the azimuth pass reads
     // next, which should stay cacheable.
     constexpr bool NT = K::NTROW && !K::COLS && EPI == EPI_NONE;
+    if (blockIdx.y) {  // several independent problems along the grid's second axis
+        in = reinterpret_cast<const char *>(in) + (long long)blockIdx.y * a.outer_in_dist * Store<IN_ST>::BYTES;
+        out = reinterpret_cast<char *>(out) + (long long)blockIdx.y * a.outer_out_dist * Store<OUT_ST>::BYTES;
+    }
     const int tid = threadIdx.x;
     const int c = K::COLS ? (tid & (K::C - 1)) : (tid >> K::LOG_T);
     const int t = K::COLS ? (tid >> K::LOG_C) : (tid & (K::T - 1));
@@ -651,7 +655,24 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
             load_points<K, IN_ST>(v, in, blk, c, t, valid, a);
             transform<K, INV, EPI, true>(v, t, c, tw, spec, a.scale, lds);
         }
-        if constexpr (EPI == EPI_RCMC || EPI == EPI_SCALE) {
+        if constexpr (EPI == EPI_TWIDDLE) {
+            // four-step: point k1 = t + T*i of column n2 times W_N^(n2 k1)
+            // = W_N^(n2 t) * W_N^(n2 T i).  Each factor is looked up exactly
+            // (W^m = lo[m mod S] * hi[m div S], n2 k1 < N): the first once per
+            // thread, the second shared by the lanes of a column (a broadcast
+            // read), instead of a scattered pair of reads per point.
+            const float2 *lo = spec, *hi = spec + (1 << a.aux);
+            const int mask = (1 << a.aux) - 1;
+            const int n2 = (int)(blk * K::C) + (valid ? c : 0);
+            const int m0 = n2 * t;
+            const float2 base = cmul(lo[m0 & mask], hi[m0 >> a.aux]);
+            static_for<0, K::P>([&](auto ic) {
+                const int m = n2 * (K::T * decltype(ic)::value);
+                const float2 w = cmul(base, cmul(lo[m & mask], hi[m >> a.aux]));
+                v[ic] = INV ? cmulc(v[ic], w) : cmul(v[ic], w);
+            });
+        }
+        if constexpr (EPI == EPI_RCMC || EPI == EPI_SCALE || EPI == EPI_TWIDDLE) {
             // input and output run along different axes of the image
             store_remapped<K, OUT_ST>(v, out, blk, c, t, a, lds);
         } else {
@@ -700,7 +721,9 @@ hipError_t launch_one(const void *in, void *out, const float2 *tw, const float2 
         }
         if (blocks > resident.load(std::memory_order_relaxed)) blocks = resident.load(std::memory_order_relaxed);
     }
-    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(K::THREADS), 0, stream, in, out, tw, spec, a);
+    const unsigned outer = a.outer > 1 ? (unsigned)a.outer : 1u;
+    if (outer > 1 && K::PERSIST) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks, outer), dim3(K::THREADS), 0, stream, in, out, tw, spec, a);
     return hipGetLastError();
 }
 

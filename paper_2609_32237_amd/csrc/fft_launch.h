@@ -21,7 +21,12 @@ enum { LAYOUT_ROWS = 0, LAYOUT_COLS = 1, LAYOUT_RCMC = 2 };
 //                azimuth filter), the inverse transform runs, and the result
 //                is written as columns; `spec` points to the range-Doppler
 //                tables below.
-enum { EPI_NONE = 0, EPI_MATCHED = 1, EPI_SCALE = 2, EPI_RCMC = 3 };
+//   EPI_TWIDDLE  first pass of a four-step transform of length N = N1 * N2:
+//                the column FFT of length N1, point k1 of column n2 times
+//                W_N^(n2 k1) (conjugate for the inverse), written as rows;
+//                `spec` holds W_N^m for m < S followed by W_N^(S m) for
+//                m < N / S, with S = 2^aux.
+enum { EPI_NONE = 0, EPI_MATCHED = 1, EPI_SCALE = 2, EPI_RCMC = 3, EPI_TWIDDLE = 4 };
 
 // Range-Doppler tables, one device block in this order (byte offsets from
 // rd_tables_layout; the interpolator rows are copied in from `interp_src`):
@@ -57,6 +62,10 @@ struct KArgs {
     unsigned in_span;      // bytes one workgroup's input occupies (buffer addressing)
     unsigned out_span;     // bytes one workgroup's output occupies
     long long out_stride;  // elements between points of a transform in the output; 0: same as the input
+    long long outer_in_dist;   // elements between the problems of blockIdx.y (input)
+    long long outer_out_dist;  // elements between the problems of blockIdx.y (output)
+    int outer;                 // problems along blockIdx.y (0 or 1: one)
+    int aux;                   // EPI_TWIDDLE: log2 of the low twiddle table's length
 };
 
 // Fills the addressing fields of `a` for workgroups of `c` transforms of `n`
@@ -82,6 +91,10 @@ inline void set_spans(KArgs &a, long long n, long long c, int in_bytes, int out_
                                const void *in, void *out, const float2 *tw, const float2 *spec,         \
                                const KArgs &a, hipStream_t s);                                           \
     int variants_n##N(int layout);
+MI355FFT_DECLARE_LAUNCH(64)
+MI355FFT_DECLARE_LAUNCH(128)
+MI355FFT_DECLARE_LAUNCH(256)
+MI355FFT_DECLARE_LAUNCH(512)
 MI355FFT_DECLARE_LAUNCH(1024)
 MI355FFT_DECLARE_LAUNCH(2048)
 MI355FFT_DECLARE_LAUNCH(4096)

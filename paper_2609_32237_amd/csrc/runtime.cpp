@@ -23,15 +23,26 @@ struct fft_plan {
     int64_t n, batch, stride, dist;
     int storage, dir, device, layout, xcd_remap, variant;
     const float2 *tw;
+    // four-step (n > 16384): n = n1 * n2; pass 1 runs n2 columns of length n1,
+    // pass 2 n1 columns of length n2
+    int64_t n1, n2;
+    int log2s, v1, v2;
+    const float2 *tw1, *tw2, *ftab;
 };
 
 namespace {
 
-constexpr int64_t kMinN = 1024, kMaxN = 16384;
+constexpr int64_t kMinN = 1024, kMaxN = 16384;      // single-pass transforms
+constexpr int64_t kMaxFourStep = int64_t(1) << 28;  // two passes: n1 * n2, each <= 16384
 constexpr int64_t kMaxIndex = int64_t(1) << 40;  // largest element index accepted
 
 bool is_pow2(int64_t n) { return n > 0 && (n & (n - 1)) == 0; }
 bool supported_n(int64_t n) { return is_pow2(n) && n >= kMinN && n <= kMaxN; }
+int ilog2(int64_t n) {
+    int l = 0;
+    while ((int64_t(1) << (l + 1)) <= n) ++l;
+    return l;
+}
 
 bool fail_alloc_hook() {
     const char *e = std::getenv("MI355FFT_TEST_FAIL_ALLOC");
@@ -143,10 +154,52 @@ int get_interp(int device, const float2 **out) {
     return FFT_OK;
 }
 
+// Four-step twiddles W_N^m = exp(-2 pi i m / N), m < N, as two tables of
+// about sqrt(N) entries: lo[m] = W_N^m for m < S, hi[m] = W_N^(S m) for
+// m < N / S (S = 2^ceil(log2(N) / 2)), each computed in double with the
+// angle 2 pi (m / N) and rounded once; W_N^m = lo[m mod S] * hi[m div S].
+std::mutex g_ftab_mutex;
+std::map<std::pair<int, int64_t>, float2 *> g_ftab;
+
+int get_fourstep_table(int device, int64_t n, int log2s, const float2 **out) {
+    std::lock_guard<std::mutex> lock(g_ftab_mutex);
+    auto it = g_ftab.find({device, n});
+    if (it != g_ftab.end()) {
+        *out = it->second;
+        return FFT_OK;
+    }
+    const int64_t s = int64_t(1) << log2s, h = n / s;
+    std::vector<float2> host((size_t)(s + h));
+    const double two_pi = 6.283185307179586476925286766559;
+    for (int64_t m = 0; m < s; ++m) {
+        const double ang = two_pi * ((double)m / (double)n);
+        host[(size_t)m] = make_float2((float)std::cos(ang), (float)-std::sin(ang));
+    }
+    for (int64_t m = 0; m < h; ++m) {
+        const double ang = two_pi * ((double)(m * s) / (double)n);
+        host[(size_t)(s + m)] = make_float2((float)std::cos(ang), (float)-std::sin(ang));
+    }
+    float2 *dev = nullptr;
+    hipError_t e = hipMalloc((void **)&dev, sizeof(float2) * host.size());
+    if (e != hipSuccess) return map_hip(e);
+    e = hipMemcpy(dev, host.data(), sizeof(float2) * host.size(), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        (void)hipFree(dev);
+        return map_hip(e);
+    }
+    g_ftab[{device, n}] = dev;
+    *out = dev;
+    return FFT_OK;
+}
+
 hipError_t launch_fft(int64_t n, int variant, int layout, int in_st, int out_st, int inv, int epi, const void *in,
                       void *out, const float2 *tw, const float2 *spec, const KArgs &a, hipStream_t s) {
     using namespace mi355fft;
     switch (n) {
+        case 64: return launch_fft_n64(variant, layout, in_st, out_st, inv, epi, in, out, tw, spec, a, s);
+        case 128: return launch_fft_n128(variant, layout, in_st, out_st, inv, epi, in, out, tw, spec, a, s);
+        case 256: return launch_fft_n256(variant, layout, in_st, out_st, inv, epi, in, out, tw, spec, a, s);
+        case 512: return launch_fft_n512(variant, layout, in_st, out_st, inv, epi, in, out, tw, spec, a, s);
         case 1024: return launch_fft_n1024(variant, layout, in_st, out_st, inv, epi, in, out, tw, spec, a, s);
         case 2048: return launch_fft_n2048(variant, layout, in_st, out_st, inv, epi, in, out, tw, spec, a, s);
         case 4096: return launch_fft_n4096(variant, layout, in_st, out_st, inv, epi, in, out, tw, spec, a, s);
@@ -159,6 +212,10 @@ hipError_t launch_fft(int64_t n, int variant, int layout, int in_st, int out_st,
 int variant_count(int64_t n, int layout) {
     using namespace mi355fft;
     switch (n) {
+        case 64: return variants_n64(layout);
+        case 128: return variants_n128(layout);
+        case 256: return variants_n256(layout);
+        case 512: return variants_n512(layout);
         case 1024: return variants_n1024(layout);
         case 2048: return variants_n2048(layout);
         case 4096: return variants_n4096(layout);
@@ -184,6 +241,22 @@ int chosen_variant(int64_t n, int layout) {
 }
 
 bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// Largest batch of n-point transforms (4096 <= n <= 16384) run in the two-pass
+// split form when out of place.  Measured on MI355X (event time of one call):
+// at n = 16384 the split takes 15-17 us for 1-16 transforms against 17.6-18 us
+// in one pass; at 4096 and 8192 one pass is always faster.  The tuning knob
+// MI355FFT_SPLIT_BATCH overrides the limit for every n; a forced row shape
+// (MI355FFT_ROW_VARIANT) turns the split off.
+int64_t split_batch(int64_t n) {
+    const char *rv = std::getenv("MI355FFT_ROW_VARIANT");
+    if (rv && rv[0]) return 0;
+    const char *e = std::getenv("MI355FFT_SPLIT_BATCH");
+    if (!e || !e[0]) return n == 16384 ? 16 : 0;
+    char *end = nullptr;
+    const long long v = std::strtoll(e, &end, 10);
+    return (*end == '\0' && v > 0) ? v : 0;
+}
 
 bool overlaps(const void *a, size_t na, const void *b, size_t nb) {
     const char *pa = (const char *)a, *pb = (const char *)b;
@@ -216,7 +289,14 @@ int fft_plan_create(int64_t n, int64_t batch, int64_t stride, int64_t dist, int 
     if (storage != FFT_STORAGE_FP32 && storage != FFT_STORAGE_FP16) return FFT_EINVAL;
     if (dir != FFT_FORWARD && dir != FFT_INVERSE) return FFT_EINVAL;
     if (n < 1 || batch < 1 || stride < 1 || dist < 1) return FFT_EINVAL;
-    if (!supported_n(n)) return FFT_EUNSUPPORTED;
+    // Transforms longer than 16384 take the four-step form.  A short batch of
+    // 4096..16384-point transforms may take it too when run out of place
+    // (Section VI: split one transform over several workgroups when the batch
+    // is too small to fill the device): at most split_batch() transforms.
+    const bool four_step = is_pow2(n) && n > kMaxN && n <= kMaxFourStep;
+    const bool may_split = is_pow2(n) && n >= 4096 && n <= kMaxN && stride == 1 && batch <= split_batch(n);
+    if (!supported_n(n) && !four_step) return FFT_EUNSUPPORTED;
+    if (four_step && stride != 1) return FFT_EUNSUPPORTED;  // long transforms: contiguous only
     // extent of the layout must be addressable
     if (batch - 1 > kMaxIndex / dist || n - 1 > kMaxIndex / stride ||
         (batch - 1) * dist > kMaxIndex - (n - 1) * stride)
@@ -227,18 +307,39 @@ int fft_plan_create(int64_t n, int64_t batch, int64_t stride, int64_t dist, int 
     if (!blocks && !interleaved) return FFT_EINVAL;
     if (batch > (int64_t)0x7fffffff) return FFT_EUNSUPPORTED;  // grid size limit
     const int layout = stride == 1 ? mi355fft::LAYOUT_ROWS : mi355fft::LAYOUT_COLS;
-    const int variant = chosen_variant(n, layout);
-    if (variant == -2) return FFT_EINVAL;
+    // four-step split: n2 = 2^floor(log2 n / 2), n1 = n / n2 (both in [128, 16384])
+    const bool split = four_step || may_split;
+    const int64_t n2 = split ? int64_t(1) << (ilog2(n) / 2) : 0, n1 = split ? n / n2 : 0;
+    const int variant = four_step ? -1 : chosen_variant(n, layout);
+    const int v1 = split ? chosen_variant(n1, mi355fft::LAYOUT_COLS) : -1;
+    const int v2 = split ? chosen_variant(n2, mi355fft::LAYOUT_COLS) : -1;
+    if (variant == -2 || v1 == -2 || v2 == -2) return FFT_EINVAL;
+    if (four_step && batch > (int64_t)0x7fffffff) return FFT_EUNSUPPORTED;
     if (fail_alloc_hook()) return FFT_ENOMEM;  // test hook: device allocation fails
 
     int device = 0;
     hipError_t e = hipGetDevice(&device);
     if (e != hipSuccess) return map_hip(e);
-    const float2 *tw = nullptr;
-    int rc = get_twiddles(device, n, &tw);
+    const float2 *tw = nullptr, *tw1 = nullptr, *tw2 = nullptr, *ftab = nullptr;
+    const int log2s = split ? (ilog2(n) + 1) / 2 : 0;
+    int rc = FFT_OK;
+    if (split) {
+        rc = get_twiddles(device, n1, &tw1);
+        if (rc == FFT_OK) rc = get_twiddles(device, n2, &tw2);
+        if (rc == FFT_OK) rc = get_fourstep_table(device, n, log2s, &ftab);
+    }
+    if (rc == FFT_OK && !four_step) rc = get_twiddles(device, n, &tw);
     if (rc != FFT_OK) return rc;
     fft_plan *p = new (std::nothrow) fft_plan;
     if (!p) return FFT_ENOMEM;
+    p->n1 = n1;
+    p->n2 = n2;
+    p->log2s = log2s;
+    p->v1 = v1;
+    p->v2 = v2;
+    p->tw1 = tw1;
+    p->tw2 = tw2;
+    p->ftab = ftab;
     p->n = n;
     p->batch = batch;
     p->stride = stride;
@@ -258,6 +359,37 @@ int fft_execute(const fft_plan *plan, const void *in, void *out, hipStream_t str
     if (!plan || !in || !out) return FFT_EINVAL;
     const size_t el = plan->storage == FFT_STORAGE_FP32 ? 8 : 4;
     if (!aligned(in, el) || !aligned(out, el)) return FFT_EALIGN;
+    if (plan->n1 && (plan->n > kMaxN || in != out)) {
+        // four-step (Section VI's two-pass transform for lengths beyond the
+        // chip): pass 1 transforms the n2 columns of length n1 of each
+        // problem viewed as an n1 x n2 matrix, multiplies point k1 of column
+        // n2 by W_N^(n2 k1) and writes the columns as rows of `out`; pass 2
+        // transforms, in place, the n1 columns of length n2 of that n2 x n1
+        // matrix, which leaves X[k1 + n1 k2] in natural order.
+        if (in == out) return FFT_EINVAL;
+        const int inv = plan->dir == FFT_INVERSE;
+        const int64_t n1 = plan->n1, n2 = plan->n2;
+        for (int64_t b0 = 0; b0 < plan->batch; b0 += 65535) {
+            const int64_t nb = plan->batch - b0 < 65535 ? plan->batch - b0 : 65535;
+            const char *pin = (const char *)in + (size_t)(b0 * plan->dist) * el;
+            char *pout = (char *)out + (size_t)(b0 * plan->dist) * el;
+            KArgs a1{n2, n2, 1, n1, 1.0f, 1};
+            a1.out_stride = 1;
+            a1.outer = (int)nb;
+            a1.outer_in_dist = a1.outer_out_dist = plan->dist;
+            a1.aux = plan->log2s;
+            hipError_t e = launch_fft(n1, plan->v1, mi355fft::LAYOUT_COLS, plan->storage, plan->storage, inv,
+                                      mi355fft::EPI_TWIDDLE, pin, pout, plan->tw1, plan->ftab, a1, stream);
+            if (e != hipSuccess) return map_hip(e);
+            KArgs a2{n1, n1, 1, 1, 1.0f, 1};
+            a2.outer = (int)nb;
+            a2.outer_in_dist = a2.outer_out_dist = plan->dist;
+            e = launch_fft(n2, plan->v2, mi355fft::LAYOUT_COLS, plan->storage, plan->storage, inv,
+                           mi355fft::EPI_NONE, pout, pout, plan->tw2, nullptr, a2, stream);
+            if (e != hipSuccess) return map_hip(e);
+        }
+        return FFT_OK;
+    }
     const KArgs a{plan->batch, plan->stride, plan->dist, plan->dist, 1.0f, plan->xcd_remap};
     const int inv = plan->dir == FFT_INVERSE;
     return map_hip(launch_fft(plan->n, plan->variant, plan->layout, plan->storage, plan->storage, inv,

@@ -19,6 +19,7 @@ import workloads
 pytestmark = pytest.mark.filterwarnings("ignore::RuntimeWarning")
 
 SIZES = [1024, 2048, 4096, 8192, 16384]
+LONG = [1 << 15, 1 << 17, 1 << 20]  # four-step lengths (the oracle's radix-2 takes any power of two)
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 
@@ -74,7 +75,7 @@ def test_fft_vs_bruteforce(oracle_mod, n):
             assert rel(oracle_mod.fft(x, sign), oracle_mod.dft_direct(x, sign)) < 1e-12
 
 
-@pytest.mark.parametrize("n", SIZES)
+@pytest.mark.parametrize("n", SIZES + LONG)
 def test_fft_closed_forms(oracle_mod, n):
     k = np.arange(n)
     rng = np.random.default_rng(n + 1)
@@ -117,7 +118,7 @@ def test_fft_parseval_linearity_shift_roundtrip(oracle_mod, n):
     np.testing.assert_allclose(oracle_mod.fft(y, +1), n * x, atol=1e-9)
 
 
-@pytest.mark.parametrize("n", SIZES)
+@pytest.mark.parametrize("n", SIZES + LONG)
 def test_fft_vs_numpy(oracle_mod, n):
     rng = np.random.default_rng(3 * n)
     x = rand_c(rng, 3, n)
