@@ -106,6 +106,32 @@ typedef struct fft_plan fft_plan; /* opaque; immutable once created */
 int fft_plan_create(int64_t n, int64_t batch, int64_t stride, int64_t dist, int storage, int dir,
                     fft_plan **plan_out);
 
+/* Plan flags of fft_plan_create_ex. */
+enum { FFT_FLAG_FP16_EXCHANGE = 1 };
+
+/*
+ * fft_plan_create_ex -- fft_plan_create with a fixed-shift output scale and
+ * options (Section VII: FFT outputs grow up to N for coherent data, so FP16
+ * storage of real signals needs block-floating-point scaling; Section X
+ * applies it as fixed power-of-two shifts).
+ *
+ *   scale_log2  the outputs are multiplied by 2^-scale_log2, in [0, 60], else
+ *               FFT_EINVAL.  The product is exact in FP32 (no rounding), so
+ *               the caller keeps the block exponent: scale_log2 = log2(n)
+ *               bounds every output of a forward transform by the largest
+ *               input magnitude, whatever the data.  0 is fft_plan_create.
+ *   flags       0, or FFT_FLAG_FP16_EXCHANGE: the exchange between stages is
+ *               stored as binary16 pairs instead of FP32 (Section VII's
+ *               FP16-exchange variant: half the on-chip traffic of the FP32
+ *               exchange in one round, about 6 dB less accurate).  Requires
+ *               FFT_STORAGE_FP16 (else FFT_EINVAL), stride == 1 and
+ *               n <= 16384 (else FFT_EUNSUPPORTED).  Unknown flags give
+ *               FFT_EINVAL.
+ * Other arguments, tables and errors as fft_plan_create.
+ */
+int fft_plan_create_ex(int64_t n, int64_t batch, int64_t stride, int64_t dist, int storage, int dir,
+                       int scale_log2, unsigned flags, fft_plan **plan_out);
+
 /*
  * fft_execute -- run the planned transforms: out = FFT(in).
  *

@@ -25,7 +25,9 @@ FFT_EALIGN = -4
 FFT_EHIP = -5
 
 # every symbol include/mi355fft.h declares
-EXPORTS = ("fft_plan_create", "fft_execute", "fft_plan_destroy", "sar_workspace_bytes",
+FFT_FLAG_FP16_EXCHANGE = 1
+
+EXPORTS = ("fft_plan_create", "fft_plan_create_ex", "fft_execute", "fft_plan_destroy", "sar_workspace_bytes",
            "sar_form_image_ex", "sar_form_image", "sar_rd_workspace_bytes", "sar_rd_form_image",
            "fft_strerror")
 
@@ -45,6 +47,8 @@ lib = ctypes.CDLL(LIB_PATH)
 _i64, _vp, _int = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
 lib.fft_plan_create.argtypes = [_i64, _i64, _i64, _i64, _int, _int, ctypes.POINTER(_vp)]
 lib.fft_plan_create.restype = _int
+lib.fft_plan_create_ex.argtypes = [_i64, _i64, _i64, _i64, _int, _int, _int, ctypes.c_uint, ctypes.POINTER(_vp)]
+lib.fft_plan_create_ex.restype = _int
 lib.fft_execute.argtypes = [_vp, _vp, _vp, _vp]
 lib.fft_execute.restype = _int
 lib.fft_plan_destroy.argtypes = [_vp]
@@ -83,6 +87,15 @@ def fft_plan_create(n: int, batch: int, stride: int, dist: int, storage: int, di
     """Returns an opaque plan handle (int); raises FFTError on failure."""
     p = _vp()
     _check(lib.fft_plan_create(n, batch, stride, dist, storage, dir, ctypes.byref(p)), "fft_plan_create")
+    return p.value
+
+
+def fft_plan_create_ex(n: int, batch: int, stride: int, dist: int, storage: int, dir: int, scale_log2: int = 0,
+                       flags: int = 0) -> int:
+    """fft_plan_create with the output scale 2^-scale_log2 and plan flags."""
+    p = _vp()
+    _check(lib.fft_plan_create_ex(n, batch, stride, dist, storage, dir, scale_log2, flags, ctypes.byref(p)),
+           "fft_plan_create_ex")
     return p.value
 
 

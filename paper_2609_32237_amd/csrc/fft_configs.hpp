@@ -34,6 +34,7 @@ struct Configs<64> {
     using Rows = KList<KCfg<64, 16, 16, false, XCHG_SPLIT, 1, false, Radices<16, 4>>>;
     using Cols = KList<KCfg<64, 16, 64, true, XCHG_SPLIT, 1, false, Radices<16, 4>>>;
     using Rcmc = Rows;
+    using RowsHalf = Rows;
     static constexpr int kRowDefault[2] = {0, 0}, kColDefault[2] = {0, 0};
     static constexpr int kRowMatched = 0, kColMatched = 0;
 };
@@ -42,6 +43,7 @@ struct Configs<128> {
     using Rows = KList<KCfg<128, 16, 16, false, XCHG_SPLIT, 1, false, Radices<16, 8>>>;
     using Cols = KList<KCfg<128, 16, 32, true, XCHG_SPLIT, 1, false, Radices<16, 8>>>;
     using Rcmc = Rows;
+    using RowsHalf = Rows;
     static constexpr int kRowDefault[2] = {0, 0}, kColDefault[2] = {0, 0};
     static constexpr int kRowMatched = 0, kColMatched = 0;
 };
@@ -50,6 +52,7 @@ struct Configs<256> {
     using Rows = KList<KCfg<256, 16, 16, false, XCHG_SPLIT, 1, false, Radices<16, 16>>>;
     using Cols = KList<KCfg<256, 16, 16, true, XCHG_SPLIT, 1, false, Radices<16, 16>>>;
     using Rcmc = Rows;
+    using RowsHalf = Rows;
     static constexpr int kRowDefault[2] = {0, 0}, kColDefault[2] = {0, 0};
     static constexpr int kRowMatched = 0, kColMatched = 0;
 };
@@ -60,6 +63,7 @@ struct Configs<512> {
     using Cols = KList<KCfg<512, 16, 16, true, XCHG_SPLIT, 1, false, Radices<16, 16, 2>>,
                        KCfg<512, 16, 8, true, XCHG_SPLIT, 1, false, Radices<16, 16, 2>>>;
     using Rcmc = Rows;
+    using RowsHalf = Rows;
     static constexpr int kRowDefault[2] = {0, 0}, kColDefault[2] = {0, 0};
     static constexpr int kRowMatched = 0, kColMatched = 0;
 };
@@ -73,6 +77,7 @@ struct Configs<1024> {
                        KCfg<1024, 16, 8, true, XCHG_FULL, 0, false, Radices<16, 16, 4>>>;
     using Rcmc = KList<KCfg<1024, 16, 16, false, XCHG_SPLIT, 1, false, Radices<16, 16, 4>>,
                        KCfg<1024, 16, 8, false, XCHG_SPLIT, 1, false, Radices<16, 16, 4>>>;
+    using RowsHalf = KList<KCfg<1024, 16, 4, false, XCHG_HALF, 1, false, Radices<16, 16, 4>>>;
     static constexpr int kRowDefault[2] = {1, 0}, kColDefault[2] = {0, 0};
     static constexpr int kRowMatched = 1, kColMatched = 0;
 };
@@ -86,6 +91,7 @@ struct Configs<2048> {
                        KCfg<2048, 16, 4, true, XCHG_FULL, 0, false, Radices<16, 16, 8>>>;
     using Rcmc = KList<KCfg<2048, 16, 8, false, XCHG_SPLIT, 1, false, Radices<16, 16, 8>>,
                        KCfg<2048, 16, 4, false, XCHG_SPLIT, 1, false, Radices<16, 16, 8>>>;
+    using RowsHalf = KList<KCfg<2048, 16, 2, false, XCHG_HALF, 1, false, Radices<16, 16, 8>>>;
     static constexpr int kRowDefault[2] = {0, 0}, kColDefault[2] = {0, 0};
     static constexpr int kRowMatched = 0, kColMatched = 0;
 };
@@ -106,6 +112,7 @@ struct Configs<4096> {
     // matched-filter column pass spills with them and keeps 4-column strips
     using Rcmc = KList<KCfg<4096, 32, 8, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>,
                        KCfg<4096, 16, 4, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>>;
+    using RowsHalf = KList<KCfg<4096, 16, 1, false, XCHG_HALF, 1, false, Radices<16, 16, 16>>>;
     static constexpr int kRowDefault[2] = {0, 1}, kColDefault[2] = {3, 3};
     static constexpr int kRowMatched = 1, kColMatched = 0;
 };
@@ -119,6 +126,7 @@ struct Configs<8192> {
                        KCfg<8192, 32, 2, true, XCHG_SPLIT, 0, false, Radices<16, 16, 16, 2>>>;
     using Rcmc = KList<KCfg<8192, 32, 4, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 2>>,
                        KCfg<8192, 16, 2, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 2>>>;
+    using RowsHalf = KList<KCfg<8192, 16, 1, false, XCHG_HALF, 1, false, Radices<16, 16, 16, 2>>>;
     static constexpr int kRowDefault[2] = {0, 0}, kColDefault[2] = {0, 0};
     static constexpr int kRowMatched = 0, kColMatched = 0;
 };
@@ -133,6 +141,9 @@ struct Configs<16384> {
     static constexpr int kRowDefault[2] = {1, 0}, kColDefault[2] = {1, 1};
     using Rcmc = KList<KCfg<16384, 32, 2, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 4>>,
                        KCfg<16384, 16, 1, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 4>>>;
+    // binary16 exchange: 32 points per thread measured 8% faster than 16
+    using RowsHalf = KList<KCfg<16384, 32, 1, false, XCHG_HALF, 1, false, Radices<16, 16, 16, 4>>,
+                           KCfg<16384, 16, 1, false, XCHG_HALF, 1, false, Radices<16, 16, 16, 4>>>;
     static constexpr int kRowMatched = 1, kColMatched = 1;
 };
 
@@ -167,8 +178,8 @@ hipError_t with_variant(int idx, KList<K, Ks...>, F &&f) {
 //               inverse, read FP32 or FP16, write FP32 columns (migration
 //               correction, azimuth filter and azimuth inverse FFT).
 template <class K>
-hipError_t dispatch_cfg(int in_st, int out_st, int inv, int epi, const void *in, void *out, const float2 *tw,
-                        const float2 *spec, const KArgs &a, hipStream_t s) {
+hipError_t dispatch_cfg_full(int in_st, int out_st, int inv, int epi, const void *in, void *out, const float2 *tw,
+                             const float2 *spec, const KArgs &a, hipStream_t s) {
     if (epi == EPI_NONE) {
         if (in_st != out_st) return hipErrorInvalidValue;
         if (in_st == 0)
@@ -212,6 +223,19 @@ hipError_t dispatch_cfg(int in_st, int out_st, int inv, int epi, const void *in,
 }
 
 template <class K>
+hipError_t dispatch_cfg(int in_st, int out_st, int inv, int epi, const void *in, void *out, const float2 *tw,
+                        const float2 *spec, const KArgs &a, hipStream_t s) {
+    if constexpr (K::XCHG == XCHG_HALF) {
+        // the binary16 exchange: FP16 storage, plain transforms only
+        if (epi != EPI_NONE || in_st != 1 || out_st != 1) return hipErrorInvalidValue;
+        return inv ? launch_one<K, 1, 1, true, EPI_NONE>(in, out, tw, spec, a, s)
+                   : launch_one<K, 1, 1, false, EPI_NONE>(in, out, tw, spec, a, s);
+    } else {
+        return dispatch_cfg_full<K>(in_st, out_st, inv, epi, in, out, tw, spec, a, s);
+    }
+}
+
+template <class K>
 hipError_t dispatch_rcmc(int in_st, int out_st, int inv, const void *in, void *out, const float2 *tw,
                          const float2 *spec, const KArgs &a, hipStream_t s) {
     if (!inv || out_st != 0) return hipErrorInvalidValue;
@@ -223,6 +247,13 @@ template <int N>
 hipError_t dispatch(int variant, int layout, int in_st, int out_st, int inv, int epi, const void *in, void *out,
                     const float2 *tw, const float2 *spec, const KArgs &a, hipStream_t s) {
     auto f = [&](auto k) { return dispatch_cfg<decltype(k)>(in_st, out_st, inv, epi, in, out, tw, spec, a, s); };
+    if (layout == LAYOUT_ROWS_HALF) {
+        if constexpr (N >= 1024) {
+            return with_variant(variant >= 0 ? variant : 0, typename Configs<N>::RowsHalf{}, f);
+        } else {
+            return hipErrorInvalidValue;
+        }
+    }
     if (layout == LAYOUT_RCMC) {
         if constexpr (N >= 1024) {
             if (epi != EPI_RCMC) return hipErrorInvalidValue;
@@ -246,7 +277,8 @@ template <int N>
 int variant_count(int layout) {
     return layout == LAYOUT_ROWS   ? KListSize<typename Configs<N>::Rows>::value
            : layout == LAYOUT_COLS ? KListSize<typename Configs<N>::Cols>::value
-                                   : KListSize<typename Configs<N>::Rcmc>::value;
+           : layout == LAYOUT_RCMC ? KListSize<typename Configs<N>::Rcmc>::value
+                                   : KListSize<typename Configs<N>::RowsHalf>::value;
 }
 
 }  // namespace mi355fft

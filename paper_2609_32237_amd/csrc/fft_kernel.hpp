@@ -20,7 +20,10 @@
 // Variants (all compute the same transform; tests force each one):
 //   XCHG   FULL: complex exchange through LDS (N*8 bytes per transform);
 //          SPLIT: one real component at a time (N*4 bytes, twice the rounds;
-//          the paper's Section VI exchange, here used to double occupancy).
+//          the paper's Section VI exchange, here used to double occupancy);
+//          HALF: the complex value rounded to a binary16 pair (N*4 bytes, one
+//          round; Section VII's FP16 exchange, about 6 dB less accurate, for
+//          FP16 storage only).
 //   TWMODE 0: every inter-stage twiddle read from the table;
 //          1: one table read per base-4 digit of the radix, the rest formed
 //          by complex products (fewer loads, a few more FP32 operations).
@@ -43,7 +46,7 @@
 
 namespace mi355fft {
 
-enum { XCHG_FULL = 0, XCHG_SPLIT = 1 };
+enum { XCHG_FULL = 0, XCHG_SPLIT = 1, XCHG_HALF = 2 };
 
 
 template <int... Rs>
@@ -221,6 +224,22 @@ __device__ __forceinline__ void exchange(float2 (&v)[K::P], int t, int c, float 
             constexpr int i = decltype(ic)::value;
             v[i] = L[rbase + lds_offset<K>(T * i)];
         });
+    } else if constexpr (K::XCHG == XCHG_HALF) {
+        // the complex value as a binary16 pair (round to nearest even)
+        unsigned *L = reinterpret_cast<unsigned *>(lds);
+        if constexpr (!FIRST) __syncthreads();
+        static_for<0, B>([&](auto qc) {
+            constexpr int q = decltype(qc)::value;
+            static_for<0, R>([&](auto rc) {
+                constexpr int r = decltype(rc)::value;
+                L[wbase + lds_offset<K>(q * T * R + r * NS)] = Store<1>::narrow(v[q + r * B]);
+            });
+        });
+        __syncthreads();
+        static_for<0, P>([&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            v[i] = Store<1>::widen(L[rbase + lds_offset<K>(T * i)]);
+        });
     } else {
         // one real component at a time: half the LDS, twice the rounds
         if constexpr (!FIRST) __syncthreads();
@@ -233,6 +252,7 @@ __device__ __forceinline__ void exchange(float2 (&v)[K::P], int t, int c, float 
         });
         __syncthreads();
         float re[P];
+        static_assert(K::XCHG == XCHG_SPLIT, "exchange mode");
         static_for<0, P>([&](auto ic) {
             constexpr int i = decltype(ic)::value;
             re[i] = lds[rbase + lds_offset<K>(T * i)];
@@ -574,6 +594,8 @@ __device__ __forceinline__ void store_remapped(float2 (&v)[K::P], void *__restri
         __syncthreads();
         static_for<0, P>([&](auto ic) { v[ic] = L[rbase + lds_offset<K>(T * decltype(ic)::value)]; });
     } else {
+        // one real component at a time (also for the FP16-exchange shapes: the
+        // remap moves final results, which stay exact)
         static_for<0, P>([&](auto ic) { lds[wbase + lds_offset<K>(T * decltype(ic)::value)] = v[ic].x; });
         __syncthreads();
         float re[P];
@@ -614,6 +636,15 @@ __device__ __forceinline__ void transform(float2 (&v)[K::P], int t, int c, const
             constexpr int i = decltype(ic)::value;
             v[i] = make_float2(v[i].x * scale, v[i].y * scale);
         });
+    }
+    if constexpr (EPI == EPI_NONE) {
+        // the plan's fixed-shift output scale 2^-s (exact), skipped when 1
+        if (scale != 1.0f) {
+            static_for<0, K::P>([&](auto ic) {
+                constexpr int i = decltype(ic)::value;
+                v[i] = make_float2(v[i].x * scale, v[i].y * scale);
+            });
+        }
     }
 }
 

@@ -9,7 +9,10 @@ namespace mi355fft {
 // Kernel families: contiguous rows, strided column strips, and the
 // migration-correction pass (row-mapped kernels over the transposed
 // range-Doppler image that write columns of the focused image).
-enum { LAYOUT_ROWS = 0, LAYOUT_COLS = 1, LAYOUT_RCMC = 2 };
+// The row kernels with the binary16 exchange (Section VII's FP16-exchange
+// variant: half the LDS of the FP32 exchange in one round, about 6 dB less
+// accurate) form a fourth family, for FP16 storage only.
+enum { LAYOUT_ROWS = 0, LAYOUT_COLS = 1, LAYOUT_RCMC = 2, LAYOUT_ROWS_HALF = 3 };
 // Per-kernel fusions around the transform:
 //   EPI_NONE     the plain transform;
 //   EPI_MATCHED  forward, X * conj(spec) * scale, inverse (range or azimuth

@@ -22,6 +22,7 @@ using mi355fft::KArgs;
 struct fft_plan {
     int64_t n, batch, stride, dist;
     int storage, dir, device, layout, xcd_remap, variant;
+    float scale;  // output scale 2^-s (exact)
     const float2 *tw;
     // four-step (n > 16384): n = n1 * n2; pass 1 runs n2 columns of length n1,
     // pass 2 n1 columns of length n2
@@ -232,7 +233,8 @@ int variant_count(int64_t n, int layout) {
 int chosen_variant(int64_t n, int layout) {
     const char *e = std::getenv(layout == mi355fft::LAYOUT_ROWS   ? "MI355FFT_ROW_VARIANT"
                                 : layout == mi355fft::LAYOUT_COLS ? "MI355FFT_COL_VARIANT"
-                                                                  : "MI355FFT_RCMC_VARIANT");
+                                : layout == mi355fft::LAYOUT_RCMC ? "MI355FFT_RCMC_VARIANT"
+                                                                  : "MI355FFT_HALF_VARIANT");
     if (!e || !e[0]) return -1;
     char *end = nullptr;
     long v = std::strtol(e, &end, 10);
@@ -285,16 +287,27 @@ extern "C" {
 
 int fft_plan_create(int64_t n, int64_t batch, int64_t stride, int64_t dist, int storage, int dir,
                     fft_plan **plan_out) {
+    return fft_plan_create_ex(n, batch, stride, dist, storage, dir, 0, 0u, plan_out);
+}
+
+int fft_plan_create_ex(int64_t n, int64_t batch, int64_t stride, int64_t dist, int storage, int dir,
+                       int scale_log2, unsigned flags, fft_plan **plan_out) {
     if (!plan_out) return FFT_EINVAL;
     if (storage != FFT_STORAGE_FP32 && storage != FFT_STORAGE_FP16) return FFT_EINVAL;
     if (dir != FFT_FORWARD && dir != FFT_INVERSE) return FFT_EINVAL;
     if (n < 1 || batch < 1 || stride < 1 || dist < 1) return FFT_EINVAL;
+    if (scale_log2 < 0 || scale_log2 > 60) return FFT_EINVAL;
+    if (flags & ~(unsigned)FFT_FLAG_FP16_EXCHANGE) return FFT_EINVAL;
+    const bool half_x = (flags & FFT_FLAG_FP16_EXCHANGE) != 0;
+    if (half_x && storage != FFT_STORAGE_FP16) return FFT_EINVAL;
     // Transforms longer than 16384 take the four-step form.  A short batch of
     // 4096..16384-point transforms may take it too when run out of place
     // (Section VI: split one transform over several workgroups when the batch
     // is too small to fill the device): at most split_batch() transforms.
     const bool four_step = is_pow2(n) && n > kMaxN && n <= kMaxFourStep;
-    const bool may_split = is_pow2(n) && n >= 4096 && n <= kMaxN && stride == 1 && batch <= split_batch(n);
+    const bool may_split =
+        !half_x && is_pow2(n) && n >= 4096 && n <= kMaxN && stride == 1 && batch <= split_batch(n);
+    if (half_x && (four_step || stride != 1)) return FFT_EUNSUPPORTED;  // single-pass rows only
     if (!supported_n(n) && !four_step) return FFT_EUNSUPPORTED;
     if (four_step && stride != 1) return FFT_EUNSUPPORTED;  // long transforms: contiguous only
     // extent of the layout must be addressable
@@ -306,7 +319,8 @@ int fft_plan_create(int64_t n, int64_t batch, int64_t stride, int64_t dist, int 
     const bool interleaved = stride >= (batch - 1) * dist + 1;
     if (!blocks && !interleaved) return FFT_EINVAL;
     if (batch > (int64_t)0x7fffffff) return FFT_EUNSUPPORTED;  // grid size limit
-    const int layout = stride == 1 ? mi355fft::LAYOUT_ROWS : mi355fft::LAYOUT_COLS;
+    const int layout = half_x ? mi355fft::LAYOUT_ROWS_HALF
+                              : stride == 1 ? mi355fft::LAYOUT_ROWS : mi355fft::LAYOUT_COLS;
     // four-step split: n2 = 2^floor(log2 n / 2), n1 = n / n2 (both in [128, 16384])
     const bool split = four_step || may_split;
     const int64_t n2 = split ? int64_t(1) << (ilog2(n) / 2) : 0, n1 = split ? n / n2 : 0;
@@ -332,6 +346,7 @@ int fft_plan_create(int64_t n, int64_t batch, int64_t stride, int64_t dist, int 
     if (rc != FFT_OK) return rc;
     fft_plan *p = new (std::nothrow) fft_plan;
     if (!p) return FFT_ENOMEM;
+    p->scale = std::ldexp(1.0f, -scale_log2);
     p->n1 = n1;
     p->n2 = n2;
     p->log2s = log2s;
@@ -381,7 +396,7 @@ int fft_execute(const fft_plan *plan, const void *in, void *out, hipStream_t str
             hipError_t e = launch_fft(n1, plan->v1, mi355fft::LAYOUT_COLS, plan->storage, plan->storage, inv,
                                       mi355fft::EPI_TWIDDLE, pin, pout, plan->tw1, plan->ftab, a1, stream);
             if (e != hipSuccess) return map_hip(e);
-            KArgs a2{n1, n1, 1, 1, 1.0f, 1};
+            KArgs a2{n1, n1, 1, 1, plan->scale, 1};
             a2.outer = (int)nb;
             a2.outer_in_dist = a2.outer_out_dist = plan->dist;
             e = launch_fft(n2, plan->v2, mi355fft::LAYOUT_COLS, plan->storage, plan->storage, inv,
@@ -390,7 +405,7 @@ int fft_execute(const fft_plan *plan, const void *in, void *out, hipStream_t str
         }
         return FFT_OK;
     }
-    const KArgs a{plan->batch, plan->stride, plan->dist, plan->dist, 1.0f, plan->xcd_remap};
+    const KArgs a{plan->batch, plan->stride, plan->dist, plan->dist, plan->scale, plan->xcd_remap};
     const int inv = plan->dir == FFT_INVERSE;
     return map_hip(launch_fft(plan->n, plan->variant, plan->layout, plan->storage, plan->storage, inv,
                               mi355fft::EPI_NONE, in, out, plan->tw, nullptr, a, stream));

@@ -33,11 +33,12 @@ class Plan:
     """A plan for ``batch`` transforms of ``n`` points in an advanced layout."""
 
     def __init__(self, n: int, batch: int, stride: int = 1, dist: int | None = None,
-                 storage: int = FFT_STORAGE_FP32, direction: int = FFT_FORWARD):
+                 storage: int = FFT_STORAGE_FP32, direction: int = FFT_FORWARD, scale_log2: int = 0,
+                 flags: int = 0):
         self.n, self.batch, self.stride = n, batch, stride
         self.dist = n if dist is None else dist
         self.storage, self.direction = storage, direction
-        self.handle = _lib.fft_plan_create(n, batch, stride, self.dist, storage, direction)
+        self.handle = _lib.fft_plan_create_ex(n, batch, stride, self.dist, storage, direction, scale_log2, flags)
 
     def execute(self, inp: torch.Tensor, out: torch.Tensor, stream=None) -> torch.Tensor:
         for t in (inp, out):

@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_header_declares_the_abi():
     assert declared_functions() == sorted(
-        ["fft_plan_create", "fft_execute", "fft_plan_destroy", "sar_workspace_bytes", "sar_form_image_ex",
+        ["fft_plan_create", "fft_plan_create_ex", "fft_execute", "fft_plan_destroy", "sar_workspace_bytes", "sar_form_image_ex",
          "sar_form_image", "sar_rd_workspace_bytes", "sar_rd_form_image", "fft_strerror"])
 
 
@@ -194,3 +194,18 @@ def test_long_transform_plans_are_accepted(L):
         assert rc in (L.FFT_OK, L.FFT_EHIP, L.FFT_ENOMEM), (n, rc)
         if rc == L.FFT_OK:
             L.lib.fft_plan_destroy(p)
+
+
+@pytest.mark.parametrize("args, code", [
+    ((4096, 1, 1, 4096, 0, -1, -1, 0), "FFT_EINVAL"),       # negative shift
+    ((4096, 1, 1, 4096, 0, -1, 61, 0), "FFT_EINVAL"),       # shift beyond 60
+    ((4096, 1, 1, 4096, 1, -1, 0, 2), "FFT_EINVAL"),        # unknown flag
+    ((4096, 1, 1, 4096, 0, -1, 0, 1), "FFT_EINVAL"),        # FP16 exchange needs FP16 storage
+    ((4096, 2, 2, 1, 1, -1, 0, 1), "FFT_EUNSUPPORTED"),     # FP16 exchange: rows only
+    ((32768, 1, 1, 32768, 1, -1, 0, 1), "FFT_EUNSUPPORTED"),  # FP16 exchange: single pass only
+    ((1000, 1, 1, 1000, 0, -1, 3, 0), "FFT_EUNSUPPORTED"),
+])
+def test_plan_ex_argument_errors(L, args, code):
+    p = ctypes.c_void_p()
+    assert L.lib.fft_plan_create_ex(*args, ctypes.byref(p)) == getattr(L, code)
+    assert p.value is None
