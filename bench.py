@@ -109,6 +109,29 @@ def fft_breakdown(torch, api, flush, name, samples):
             "GFLOPS": round(gflops(n, batch, med * 1e-3), 1)}
 
 
+def matrix_unit_experiment(torch, api, flush, samples):
+    """FP16 storage, 1 GiB batches: the vector kernels (FP32 exchange), the FP16
+    exchange and the radix-16 butterflies on the matrix cores (Section VIII)."""
+    res = {"experiment": "matrix-units", "storage": "fp16", "results": []}
+    g = torch.Generator(device="cuda").manual_seed(12)
+    for n in (4096, 16384):
+        batch = (1 << 30) // (n * 4)
+        x = (torch.rand(batch, n, 2, device="cuda", generator=g) * 2 - 1).half()
+        out = torch.empty_like(x)
+        for name, flags in (("vector", 0), ("fp16_exchange", api._lib.FFT_FLAG_FP16_EXCHANGE),
+                            ("matrix_units", api._lib.FFT_FLAG_MATRIX_UNITS)):
+            plan = api.Plan(n, batch, 1, n, 1, -1, flags=flags)
+            med, q1, q3 = time_samples(torch, lambda: plan.execute(x, out), flush, samples)
+            plan.close()
+            gbs = 8 * n * batch / (med * 1e-3) / 1e9
+            res["results"].append({"n": n, "batch": batch, "kernels": name, "ms_median": round(med, 5),
+                                   "ms_iqr": [round(q1, 5), round(q3, 5)], "GB/s": round(gbs, 1),
+                                   "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)})
+        del x, out
+        torch.cuda.empty_cache()
+    return res
+
+
 def long_breakdown(torch, api, flush, n, batch, samples):
     """A transform longer than the chip holds: the two-pass four-step form.
     GB/s counts the method's own 16 bytes per point (one read, one write);
@@ -299,6 +322,9 @@ def main():
     ap.add_argument("--samples", type=int, default=11, help="cache-flushed samples per breakdown workload")
     ap.add_argument("--no-breakdown", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--experiment", choices=["matrix-units"], default=None,
+                    help="instead of the benchmark: FP16-storage N = 4096 / 16384 with the vector kernels, the "
+                         "FP16 exchange and the matrix-core butterflies (one JSON line)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on one GPU; --gpus must be 1",
@@ -311,6 +337,9 @@ def main():
     from paper_2609_32237_amd import torch_api as api
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.experiment == "matrix-units":
+        print(json.dumps(matrix_unit_experiment(torch, api, Flusher(torch), args.samples)), flush=True)
+        return
     w = workloads.FFT_WORKLOADS[WORKLOAD]
     n, batch = w["n"], w["batch"]
     log(f"generating {WORKLOAD}")

@@ -107,7 +107,7 @@ int fft_plan_create(int64_t n, int64_t batch, int64_t stride, int64_t dist, int 
                     fft_plan **plan_out);
 
 /* Plan flags of fft_plan_create_ex. */
-enum { FFT_FLAG_FP16_EXCHANGE = 1 };
+enum { FFT_FLAG_FP16_EXCHANGE = 1, FFT_FLAG_MATRIX_UNITS = 2 };
 
 /*
  * fft_plan_create_ex -- fft_plan_create with a fixed-shift output scale and
@@ -125,8 +125,18 @@ enum { FFT_FLAG_FP16_EXCHANGE = 1 };
  *               FP16-exchange variant: half the on-chip traffic of the FP32
  *               exchange in one round, about 6 dB less accurate).  Requires
  *               FFT_STORAGE_FP16 (else FFT_EINVAL), stride == 1 and
- *               n <= 16384 (else FFT_EUNSUPPORTED).  Unknown flags give
- *               FFT_EINVAL.
+ *               n <= 16384 (else FFT_EUNSUPPORTED).
+ *               FFT_FLAG_MATRIX_UNITS: the radix-16 butterflies run on the
+ *               matrix cores (Section VIII: each radix-16 stage as the 32 x 32
+ *               real DFT matrix times the data, in binary16 with FP32
+ *               accumulation; the twiddles in FP32 between stages).  The data
+ *               are rounded to binary16 once per stage (the paper's matrix
+ *               kernel measured 66 dB).  Requires FFT_STORAGE_FP16 (else
+ *               FFT_EINVAL), stride == 1, n = 4096 or 16384 and scale_log2 = 0
+ *               (else FFT_EUNSUPPORTED); exclusive with the FP16 exchange.
+ *               Slower than the default kernels on MI355X (1.2x the time at
+ *               n = 4096, 1.46x at 16384, from HBM): an experiment, opt-in.
+ *               Unknown flags give FFT_EINVAL.
  * Other arguments, tables and errors as fft_plan_create.
  */
 int fft_plan_create_ex(int64_t n, int64_t batch, int64_t stride, int64_t dist, int storage, int dir,

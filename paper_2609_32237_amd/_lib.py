@@ -26,6 +26,7 @@ FFT_EHIP = -5
 
 # every symbol include/mi355fft.h declares
 FFT_FLAG_FP16_EXCHANGE = 1
+FFT_FLAG_MATRIX_UNITS = 2
 
 EXPORTS = ("fft_plan_create", "fft_plan_create_ex", "fft_execute", "fft_plan_destroy", "sar_workspace_bytes",
            "sar_form_image_ex", "sar_form_image", "sar_rd_workspace_bytes", "sar_rd_form_image",

@@ -105,4 +105,13 @@ MI355FFT_DECLARE_LAUNCH(8192)
 MI355FFT_DECLARE_LAUNCH(16384)
 #undef MI355FFT_DECLARE_LAUNCH
 
+// FP16-storage rows with the radix-16 butterflies on the matrix cores
+// (fft_mfma.hpp): one transform per workgroup, stride 1.
+// `amat` is the lane-fragment table of the 16-point DFT matrix (8 KiB, see
+// fft_mfma.hpp).
+hipError_t launch_fft_mfma_n4096(int inv, const void *in, void *out, const float2 *tw, const void *amat,
+                                 const KArgs &a, hipStream_t s);
+hipError_t launch_fft_mfma_n16384(int inv, const void *in, void *out, const float2 *tw, const void *amat,
+                                  const KArgs &a, hipStream_t s);
+
 }  // namespace mi355fft

@@ -1,5 +1,6 @@
 // fft_n16384.hip -- instantiations of the single-pass kernels for N = 16384.
 #include "fft_configs.hpp"
+#include "fft_mfma.hpp"
 
 namespace mi355fft {
 
@@ -9,5 +10,10 @@ hipError_t launch_fft_n16384(int variant, int layout, int in_st, int out_st, int
 }
 
 int variants_n16384(int layout) { return variant_count<16384>(layout); }
+
+hipError_t launch_fft_mfma_n16384(int inv, const void *in, void *out, const float2 *tw, const void *amat,
+                               const KArgs &a, hipStream_t s) {
+    return launch_mfma<MfmaCfg<16384, 4, 8>>(inv, in, out, tw, amat, a, s);
+}
 
 }  // namespace mi355fft

@@ -23,6 +23,8 @@ struct fft_plan {
     int64_t n, batch, stride, dist;
     int storage, dir, device, layout, xcd_remap, variant;
     float scale;  // output scale 2^-s (exact)
+    int mfma;     // radix-16 butterflies on the matrix cores (FP16 storage)
+    const void *amat;
     const float2 *tw;
     // four-step (n > 16384): n = n1 * n2; pass 1 runs n2 columns of length n1,
     // pass 2 n1 columns of length n2
@@ -193,6 +195,48 @@ int get_fourstep_table(int device, int64_t n, int log2s, const float2 **out) {
     return FFT_OK;
 }
 
+// Lane fragments of the real 32 x 32 matrix of the 16-point DFT for the
+// matrix-core kernels, both directions, split into binary16 hi + lo parts
+// (computed in double once per device; layout in fft_mfma.hpp).
+std::mutex g_amat_mutex;
+std::map<int, void *> g_amat;
+
+int get_dft16_matrix(int device, const void **out) {
+    std::lock_guard<std::mutex> lock(g_amat_mutex);
+    auto it = g_amat.find(device);
+    if (it != g_amat.end()) {
+        *out = it->second;
+        return FFT_OK;
+    }
+    std::vector<_Float16> host(2 * 64 * 2 * 2 * 8);
+    const double two_pi = 6.283185307179586476925286766559;
+    for (int d = 0; d < 2; ++d)
+        for (int l = 0; l < 64; ++l)
+            for (int s = 0; s < 2; ++s)
+                for (int e = 0; e < 8; ++e) {
+                    const int m = l % 32, kp = m >> 1, co = m & 1;
+                    const int k = 16 * s + 8 * (l / 32) + e, r = k >> 1, ci = k & 1;
+                    const double th = two_pi * (double)((kp * r) % 16) / 16.0;
+                    const double c = std::cos(th), sn = d ? -std::sin(th) : std::sin(th);
+                    const double f = co == 0 ? (ci == 0 ? c : sn) : (ci == 0 ? -sn : c);
+                    const _Float16 hi = (_Float16)f;
+                    const size_t base = (size_t)((((d * 64 + l) * 2 + s) * 2) * 8 + e);
+                    host[base] = hi;
+                    host[base + 8] = (_Float16)(f - (double)hi);
+                }
+    void *dev = nullptr;
+    hipError_t e = hipMalloc(&dev, sizeof(_Float16) * host.size());
+    if (e != hipSuccess) return map_hip(e);
+    e = hipMemcpy(dev, host.data(), sizeof(_Float16) * host.size(), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        (void)hipFree(dev);
+        return map_hip(e);
+    }
+    g_amat[device] = dev;
+    *out = dev;
+    return FFT_OK;
+}
+
 hipError_t launch_fft(int64_t n, int variant, int layout, int in_st, int out_st, int inv, int epi, const void *in,
                       void *out, const float2 *tw, const float2 *spec, const KArgs &a, hipStream_t s) {
     using namespace mi355fft;
@@ -297,16 +341,20 @@ int fft_plan_create_ex(int64_t n, int64_t batch, int64_t stride, int64_t dist, i
     if (dir != FFT_FORWARD && dir != FFT_INVERSE) return FFT_EINVAL;
     if (n < 1 || batch < 1 || stride < 1 || dist < 1) return FFT_EINVAL;
     if (scale_log2 < 0 || scale_log2 > 60) return FFT_EINVAL;
-    if (flags & ~(unsigned)FFT_FLAG_FP16_EXCHANGE) return FFT_EINVAL;
+    if (flags & ~(unsigned)(FFT_FLAG_FP16_EXCHANGE | FFT_FLAG_MATRIX_UNITS)) return FFT_EINVAL;
     const bool half_x = (flags & FFT_FLAG_FP16_EXCHANGE) != 0;
-    if (half_x && storage != FFT_STORAGE_FP16) return FFT_EINVAL;
+    const bool mfma = (flags & FFT_FLAG_MATRIX_UNITS) != 0;
+    if ((half_x || mfma) && storage != FFT_STORAGE_FP16) return FFT_EINVAL;
+    if (half_x && mfma) return FFT_EINVAL;
+    if (mfma && (stride != 1 || (n != 4096 && n != 16384))) return FFT_EUNSUPPORTED;
+    if (mfma && scale_log2 != 0) return FFT_EUNSUPPORTED;
     // Transforms longer than 16384 take the four-step form.  A short batch of
     // 4096..16384-point transforms may take it too when run out of place
     // (Section VI: split one transform over several workgroups when the batch
     // is too small to fill the device): at most split_batch() transforms.
     const bool four_step = is_pow2(n) && n > kMaxN && n <= kMaxFourStep;
     const bool may_split =
-        !half_x && is_pow2(n) && n >= 4096 && n <= kMaxN && stride == 1 && batch <= split_batch(n);
+        !half_x && !mfma && is_pow2(n) && n >= 4096 && n <= kMaxN && stride == 1 && batch <= split_batch(n);
     if (half_x && (four_step || stride != 1)) return FFT_EUNSUPPORTED;  // single-pass rows only
     if (!supported_n(n) && !four_step) return FFT_EUNSUPPORTED;
     if (four_step && stride != 1) return FFT_EUNSUPPORTED;  // long transforms: contiguous only
@@ -343,10 +391,14 @@ int fft_plan_create_ex(int64_t n, int64_t batch, int64_t stride, int64_t dist, i
         if (rc == FFT_OK) rc = get_fourstep_table(device, n, log2s, &ftab);
     }
     if (rc == FFT_OK && !four_step) rc = get_twiddles(device, n, &tw);
+    const void *amat = nullptr;
+    if (rc == FFT_OK && mfma) rc = get_dft16_matrix(device, &amat);
     if (rc != FFT_OK) return rc;
     fft_plan *p = new (std::nothrow) fft_plan;
     if (!p) return FFT_ENOMEM;
     p->scale = std::ldexp(1.0f, -scale_log2);
+    p->mfma = mfma;
+    p->amat = amat;
     p->n1 = n1;
     p->n2 = n2;
     p->log2s = log2s;
@@ -407,6 +459,11 @@ int fft_execute(const fft_plan *plan, const void *in, void *out, hipStream_t str
     }
     const KArgs a{plan->batch, plan->stride, plan->dist, plan->dist, plan->scale, plan->xcd_remap};
     const int inv = plan->dir == FFT_INVERSE;
+    if (plan->mfma) {
+        return map_hip(plan->n == 4096 ? mi355fft::launch_fft_mfma_n4096(inv, in, out, plan->tw, plan->amat, a, stream)
+                                       : mi355fft::launch_fft_mfma_n16384(inv, in, out, plan->tw, plan->amat, a,
+                                                                          stream));
+    }
     return map_hip(launch_fft(plan->n, plan->variant, plan->layout, plan->storage, plan->storage, inv,
                               mi355fft::EPI_NONE, in, out, plan->tw, nullptr, a, stream));
 }

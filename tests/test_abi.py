@@ -199,7 +199,12 @@ def test_long_transform_plans_are_accepted(L):
 @pytest.mark.parametrize("args, code", [
     ((4096, 1, 1, 4096, 0, -1, -1, 0), "FFT_EINVAL"),       # negative shift
     ((4096, 1, 1, 4096, 0, -1, 61, 0), "FFT_EINVAL"),       # shift beyond 60
-    ((4096, 1, 1, 4096, 1, -1, 0, 2), "FFT_EINVAL"),        # unknown flag
+    ((4096, 1, 1, 4096, 1, -1, 0, 4), "FFT_EINVAL"),        # unknown flag
+    ((4096, 1, 1, 4096, 0, -1, 0, 2), "FFT_EINVAL"),        # matrix units need FP16 storage
+    ((4096, 1, 1, 4096, 1, -1, 0, 3), "FFT_EINVAL"),        # two exclusive options
+    ((8192, 1, 1, 8192, 1, -1, 0, 2), "FFT_EUNSUPPORTED"),  # matrix units: 4096 and 16384
+    ((4096, 2, 2, 1, 1, -1, 0, 2), "FFT_EUNSUPPORTED"),     # matrix units: rows only
+    ((4096, 1, 1, 4096, 1, -1, 3, 2), "FFT_EUNSUPPORTED"),  # matrix units: no output scale
     ((4096, 1, 1, 4096, 0, -1, 0, 1), "FFT_EINVAL"),        # FP16 exchange needs FP16 storage
     ((4096, 2, 2, 1, 1, -1, 0, 1), "FFT_EUNSUPPORTED"),     # FP16 exchange: rows only
     ((32768, 1, 1, 32768, 1, -1, 0, 1), "FFT_EUNSUPPORTED"),  # FP16 exchange: single pass only

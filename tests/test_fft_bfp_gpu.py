@@ -123,3 +123,38 @@ def test_every_fp16_exchange_shape(lib):
         finally:
             os.environ.pop("MI355FFT_HALF_VARIANT", None)
         assert rel_rows(y, ref).max() < 3e-3, v
+
+
+
+@pytest.mark.parametrize("n", [4096, 16384])
+def test_matrix_unit_transforms(lib, n):
+    """FFT_FLAG_MATRIX_UNITS: radix-16 stages as MFMA products (binary16 data,
+    FP32 accumulation).  Within the FP16 bound, both directions, in place too;
+    its accuracy is reported beside the vector kernel's."""
+    import torch
+
+    x = workloads.uniform_complex(9, n, 995, "fp16")
+    f = lib.FFT_FLAG_MATRIX_UNITS
+    for direction in (-1, 1):
+        ref = oracle.fft(x, direction)
+        e_mm = rel_rows(widen(run(lib, x, n, 9, 1, n, 1, direction, flags=f)), ref)
+        e_v = rel_rows(widen(run(lib, x, n, 9, 1, n, 1, direction)), ref)
+        log(f"matrix units n={n} dir={direction}: rel {e_mm.mean():.2e} (vector {e_v.mean():.2e}), "
+            f"SQNR {-20 * np.log10(e_mm.mean()):.1f} dB")
+        assert e_mm.max() < 3e-3
+    # closed form: an impulse at n0 gives exp(-2 pi i k n0 / n) up to binary16 rounding
+    n0 = 77
+    imp = np.zeros((1, n, 2), np.float16)
+    imp[0, n0, 0] = 1.0
+    k = np.arange(n)
+    y = widen(run(lib, imp, n, 1, 1, n, 1, -1, flags=f))[0]
+    assert abs(y - np.exp(-2j * np.pi * ((k * n0) % n) / n)).max() < 2e-3
+    # in place
+    xd = to_dev(x)
+    p = lib.fft_plan_create_ex(n, 9, 1, n, 1, -1, 0, f)
+    try:
+        lib.fft_execute(p, xd.data_ptr(), xd.data_ptr(), torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+    finally:
+        lib.fft_plan_destroy(p)
+    assert rel_rows(widen(to_host(xd)), oracle.fft(x)).max() < 3e-3
