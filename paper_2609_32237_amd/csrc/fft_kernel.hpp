@@ -280,18 +280,12 @@ struct FirstOf {
 
 // One radix-R stage on sub-transforms of length NS: twiddle, butterfly in
 // registers; then (unless last) request the next stage's twiddles and
-// exchange through LDS.  With a non-null `pre` the last stage first requests
-// pre[t + T*i] into `prev` (the epilogue's reference spectrum), so those reads
-// overlap the stage's arithmetic.
-template <class K, bool INV, bool FIRST_X, bool PREFETCH, int NS, int R, int... Rest>
+// exchange through LDS.
+template <class K, bool INV, bool FIRST_X, int NS, int R, int... Rest>
 __device__ __forceinline__ void run_stages(float2 (&v)[K::P], int t, int c, const float2 *__restrict__ tw,
-                                           float *lds, const TwRegs<K, NS, R> &cur,
-                                           const float2 *__restrict__ pre, float2 (&prev)[K::P]) {
+                                           float *lds, const TwRegs<K, NS, R> &cur) {
     constexpr int P = K::P, B = P / R;
     static_assert(P % R == 0, "radix must divide points per thread");
-    if constexpr (PREFETCH && sizeof...(Rest) == 0) {
-        static_for<0, P>([&](auto ic) { prev[ic] = pre[t + K::T * decltype(ic)::value]; });
-    }
     static_for<0, B>([&](auto qc) {
         constexpr int q = decltype(qc)::value;
         float2 u[R];
@@ -312,16 +306,15 @@ __device__ __forceinline__ void run_stages(float2 (&v)[K::P], int t, int c, cons
         TwRegs<K, NS2, R2> nxt;
         tw_issue<K, NS2, R2>(nxt, t, tw);  // in flight during the exchange
         exchange<K, NS, R, FIRST_X>(v, t, c, lds);
-        run_stages<K, INV, false, PREFETCH, NS2, Rest...>(v, t, c, tw, lds, nxt, pre, prev);
+        run_stages<K, INV, false, NS2, Rest...>(v, t, c, tw, lds, nxt);
     }
 }
 
-template <class K, bool INV, bool FIRST_X, bool PREFETCH, int R1, int... Rs>
+template <class K, bool INV, bool FIRST_X, int R1, int... Rs>
 __device__ __forceinline__ void run_fft(Radices<R1, Rs...>, float2 (&v)[K::P], int t, int c,
-                                        const float2 *__restrict__ tw, float *lds,
-                                        const float2 *__restrict__ pre, float2 (&prev)[K::P]) {
+                                        const float2 *__restrict__ tw, float *lds) {
     TwRegs<K, 1, R1> none;  // the first stage has no twiddles
-    run_stages<K, INV, FIRST_X, PREFETCH, 1, R1, Rs...>(v, t, c, tw, lds, none, pre, prev);
+    run_stages<K, INV, FIRST_X, 1, R1, Rs...>(v, t, c, tw, lds, none);
 }
 
 // Blocks are dispatched round-robin over the 8 XCDs.  With xcd_remap the
@@ -616,20 +609,33 @@ template <class K, bool INV, int EPI, bool FIRST_X>
 __device__ __forceinline__ void transform(float2 (&v)[K::P], int t, int c, const float2 *__restrict__ tw,
                                           const float2 *__restrict__ spec, float scale, float *lds) {
     constexpr bool MF = EPI == EPI_MATCHED;
-    float2 h[K::P];  // reference spectrum (unused without the epilogue)
-    run_fft<K, INV, FIRST_X, MF>(typename K::Rad{}, v, t, c, tw, lds, spec, h);
+    run_fft<K, INV, FIRST_X>(typename K::Rad{}, v, t, c, tw, lds);
     if constexpr (MF) {
         // X[k] * conj(H[k]) * scale, k = t + T*i, then the inverse transform.
         // The scheduling fences keep the two transforms' register lifetimes
-        // apart (interleaving them costs occupancy).
+        // apart (interleaving them costs occupancy); H is read eight values
+        // at a time between fences, so it never needs a second register
+        // array beside X.
         __builtin_amdgcn_sched_barrier(0);
-        static_for<0, K::P>([&](auto ic) {
-            constexpr int i = decltype(ic)::value;
-            const float2 y = cmulc(v[i], h[i]);
-            v[i] = make_float2(y.x * scale, y.y * scale);
+        constexpr int HC = K::P < 8 ? K::P : 8;
+        static_for<0, K::P / HC>([&](auto jc) {
+            static_for<0, HC>([&](auto ec) {
+                constexpr int i = decltype(jc)::value * HC + decltype(ec)::value;
+                const float2 y = cmulc(v[i], spec[t + K::T * i]);
+                v[i] = make_float2(y.x * scale, y.y * scale);
+            });
+            __builtin_amdgcn_sched_barrier(0);
         });
-        __builtin_amdgcn_sched_barrier(0);
-        run_fft<K, !INV, false, false>(typename K::Rad{}, v, t, c, tw, lds, spec, h);
+        // The inverse reads the same twiddle table at the same per-lane
+        // indices as the forward transform.  Seen as equal, the compiler
+        // keeps the forward transform's loaded twiddles and index arithmetic
+        // alive across the multiply to reuse them (over 100 more VGPRs on the
+        // 8-column kernels, which then spill); passing the pointer and the
+        // lane coordinates through an empty asm statement hides the equality.
+        const float2 *tw2 = tw;
+        int t2 = t, c2 = c;
+        asm volatile("" : "+s"(tw2), "+v"(t2), "+v"(c2));
+        run_fft<K, !INV, false>(typename K::Rad{}, v, t2, c2, tw2, lds);
     }
     if constexpr (EPI == EPI_SCALE) {
         static_for<0, K::P>([&](auto ic) {
@@ -648,12 +654,11 @@ __device__ __forceinline__ void transform(float2 (&v)[K::P], int t, int c, const
     }
 }
 
-// Occupancy hint: the LDS-derived minimum, except for kernels that need more
-// registers than that leaves (persistent kernels hold a second transform;
-// column kernels with the epilogue hold the reference spectrum of a strip).
+// Occupancy hint: the LDS-derived minimum, except for persistent kernels,
+// which hold a second transform and need more registers than that leaves.
 template <class K, int EPI>
 constexpr int occupancy_hint() {
-    return (K::PERSIST || (EPI == EPI_MATCHED && K::COLS)) ? 1 : K::MIN_WAVES;
+    return K::PERSIST ? 1 : K::MIN_WAVES;
 }
 
 template <class K, int IN_ST, int OUT_ST, bool INV, int EPI>
