@@ -138,11 +138,6 @@ constexpr int lds_offset(int delta) {
 
 constexpr int num_digits4(int r) { return r <= 1 ? 0 : 1 + num_digits4((r + 3) / 4); }
 constexpr int pow4(int i) { return i == 0 ? 1 : 4 * pow4(i - 1); }
-constexpr int top_digit_part(int r) {  // r's highest base-4 digit times its place value
-    int p = 1;
-    while (p * 4 <= r) p *= 4;
-    return (r / p) * p;
-}
 
 template <class K, int NS, int R>
 struct TwRegs {
@@ -167,34 +162,56 @@ __device__ __forceinline__ void tw_issue(TwRegs<K, NS, R> &tr, int t, const floa
             } else {
                 static_for<0, TwRegs<K, NS, R>::LOADS>([&](auto ic) {
                     constexpr int i = decltype(ic)::value;
-                    tr.w[q][i] = tw[k * (pow4(i) * STR)];
+                    constexpr int step = pow4(i) * STR;  // folded here, never a device call
+                    tr.w[q][i] = tw[k * step];
                 });
             }
         });
     }
 }
 
-// Expand the reads of butterfly q into w[r] = W^{k r} for r = 1..R-1.
-template <class K, int NS, int R, int q>
-__device__ __forceinline__ void tw_expand(const TwRegs<K, NS, R> &tr, float2 (&w)[R]) {
+// Multiply u[r] by w[r] = W^{k r} (its conjugate for the inverse), r = 1..R-1.
+// With the digit-base reads (TWMODE 1), r = low + 16 h with low < 16:
+// w[low] is the product of its two base-4 digit parts and w[r] = w[low] *
+// w[16 h].  Each factor is applied as soon as it is formed, so only the digit
+// bases and one partial product are live at a time rather than all R - 1
+// factors (31 complex values at radix 32, which would spill).  The products
+// are the same, in the same order, as forming every factor first.
+template <class K, int NS, int R, int q, bool INV>
+__device__ __forceinline__ void tw_apply(const TwRegs<K, NS, R> &tr, float2 (&u)[R]) {
+    auto mul = [](float2 a, float2 w) { return INV ? cmulc(a, w) : cmul(a, w); };
     if constexpr (K::TWMODE == 0) {
-        static_for<1, R>([&](auto rc) { w[rc] = tr.w[q][rc - 1]; });
+        static_for<1, R>([&](auto rc) { u[rc] = mul(u[rc], tr.w[q][rc - 1]); });
     } else {
-        // powers of the digit bases, then products of digit parts
-        static_for<1, R>([&](auto rc) {
-            constexpr int r = decltype(rc)::value;
-            constexpr int top = top_digit_part(r);
-            if constexpr (top == r) {
-                // r = d * 4^i with d in {1, 2, 3}
-                constexpr int i = num_digits4(r + 1) - 1;
-                constexpr int base = pow4(i);
-                constexpr int d = r / base;
-                if constexpr (d == 1) w[r] = tr.w[q][i];
-                if constexpr (d == 2) w[r] = cmul(tr.w[q][i], tr.w[q][i]);
-                if constexpr (d == 3) w[r] = cmul(w[2 * base], tr.w[q][i]);
-            } else {
-                w[r] = cmul(w[r - top], w[top]);
-            }
+        constexpr int D = TwRegs<K, NS, R>::LOADS;
+        float2 b[D][3];  // b[i][d - 1] = W^{k d 4^i}
+        static_for<0, D>([&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            constexpr int base = pow4(i);
+            b[i][0] = tr.w[q][i];
+            if constexpr (2 * base < R) b[i][1] = cmul(b[i][0], b[i][0]);
+            if constexpr (3 * base < R) b[i][2] = cmul(b[i][1], b[i][0]);
+        });
+        constexpr int LOW = R < 16 ? R : 16;
+        static_for<0, LOW>([&](auto lc) {
+            constexpr int low = decltype(lc)::value;
+            constexpr int d0 = low % 4, d1 = low / 4;
+            float2 wl = make_float2(1.0f, 0.0f);
+            if constexpr (d0 != 0 && d1 != 0) wl = cmul(b[0][d0 - 1], b[1][d1 - 1]);
+            if constexpr (d0 != 0 && d1 == 0) wl = b[0][d0 - 1];
+            if constexpr (d0 == 0 && d1 != 0) wl = b[1][d1 - 1];
+            if constexpr (low != 0) u[low] = mul(u[low], wl);
+            static_for<1, (R + 15) / 16>([&](auto hc) {
+                constexpr int r = low + 16 * decltype(hc)::value;
+                if constexpr (r < R) {
+                    const float2 bh = b[2][decltype(hc)::value - 1];
+                    if constexpr (low != 0) {
+                        u[r] = mul(u[r], cmul(wl, bh));
+                    } else {
+                        u[r] = mul(u[r], bh);
+                    }
+                }
+            });
         });
     }
 }
@@ -290,14 +307,7 @@ __device__ __forceinline__ void run_stages(float2 (&v)[K::P], int t, int c, cons
         constexpr int q = decltype(qc)::value;
         float2 u[R];
         static_for<0, R>([&](auto rc) { u[rc] = v[q + rc * B]; });
-        if constexpr (NS > 1) {
-            float2 w[R];
-            tw_expand<K, NS, R, q>(cur, w);
-            static_for<1, R>([&](auto rc) {
-                constexpr int r = decltype(rc)::value;
-                u[r] = INV ? cmulc(u[r], w[r]) : cmul(u[r], w[r]);
-            });
-        }
+        if constexpr (NS > 1) tw_apply<K, NS, R, q, INV>(cur, u);
         Dft<R, INV>::run(u);
         static_for<0, R>([&](auto rc) { v[q + rc * B] = u[rc]; });
     });
@@ -470,7 +480,7 @@ __device__ __forceinline__ void rcmc_load(float2 (&v)[K::P], const void *__restr
     static_assert(!K::COLS && !K::PERSIST, "the migration correction reads rows of the transposed image");
     static_assert(kRcmcTaps == 8, "four float4 per table row");
     using S = RcmcStage<K>;
-    constexpr int EL = Store<ST>::BYTES, P = K::P, T = K::T, W = S::W;
+    constexpr int EL = Store<ST>::BYTES, P = K::P, T = K::T;
     // table row q holds {g_j, dg_j, g_j+1, dg_j+1} for j = 0, 2, 4, 6 in four
     // float4 slots of a five-slot stride: consecutive rows start 20 banks
     // apart, so lanes reading different rows spread over the banks
