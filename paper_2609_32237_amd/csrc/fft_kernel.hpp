@@ -327,14 +327,25 @@ __device__ __forceinline__ void run_fft(Radices<R1, Rs...>, float2 (&v)[K::P], i
     run_stages<K, INV, FIRST_X, 1, R1, Rs...>(v, t, c, tw, lds, none);
 }
 
-// Blocks are dispatched round-robin over the 8 XCDs.  With xcd_remap the
-// logical strip of block i is chosen so that each XCD works through one
-// contiguous range of strips: strips that share cache lines then meet in the
-// same L2.
+// Blocks are dispatched round-robin over the 8 XCDs.  Strips whose pieces
+// share a 128-byte line should run on one XCD, so the line meets them in one
+// L2.  Two block -> strip maps (xcd_remap):
+//   XCD_CONTIG  each XCD works through one contiguous range of strips;
+//   XCD_GROUPS  the GROUP strips of a line run on one XCD, and successive
+//               groups go to successive XCDs, so the strips in flight spread
+//               over the whole row and its memory channels.
+// Measured on MI355X: with rows of 32 KiB the groups win (strided copies of
+// 64-byte pieces 3.37 against 3.06 TB/s; 4096-point columns 79 against
+// 86 us); with rows of 8 KiB (the four-step passes at 2^20) the contiguous
+// ranges win by 10%.  The host picks by row length.  Grids that are not a
+// multiple of 8 * GROUP keep the contiguous ranges.
+template <int GROUP>
 __device__ __forceinline__ long long logical_block(int xcd_remap) {
     const long long i = blockIdx.x, g = gridDim.x;
-    if (!xcd_remap || g < 8) return i;
-    const long long xcd = i & 7, local = i >> 3, per = g >> 3, rem = g & 7;
+    if (xcd_remap == XCD_NONE || g < 8) return i;
+    const long long xcd = i & 7, local = i >> 3;
+    if (xcd_remap == XCD_GROUPS && g % (8 * GROUP) == 0) return ((local / GROUP) * 8 + xcd) * GROUP + local % GROUP;
+    const long long per = g >> 3, rem = g & 7;
     return xcd < rem ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
 }
 
@@ -692,7 +703,11 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
     const int t = K::COLS ? (tid >> K::LOG_C) : (tid & (K::T - 1));
     float2 v[K::P];
     if constexpr (!K::PERSIST) {
-        const long long blk = logical_block(a.xcd_remap);
+        // strips per 128-byte line, from the narrower of the two sides' pieces
+        constexpr int PIECE = K::C * (Store<IN_ST>::BYTES < Store<OUT_ST>::BYTES ? Store<IN_ST>::BYTES
+                                                                                : Store<OUT_ST>::BYTES);
+        constexpr int GROUP = PIECE >= 128 ? 1 : 128 / PIECE;
+        const long long blk = logical_block<GROUP>(a.xcd_remap);
         const bool valid = blk * K::C + c < a.batch;
         if constexpr (EPI == EPI_RCMC) {
             rcmc_load<K, IN_ST>(v, in, blk, c, t, valid, a, spec, lds);

@@ -288,6 +288,11 @@ int chosen_variant(int64_t n, int layout) {
 
 bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
+// Block -> strip map for column strips whose rows are row_bytes apart: the
+// line groups spread over the XCDs for rows of 32 KiB and more, contiguous
+// ranges per XCD for shorter rows (measured on MI355X, see logical_block).
+int strip_map(int64_t row_bytes) { return row_bytes >= 32768 ? mi355fft::XCD_GROUPS : mi355fft::XCD_CONTIG; }
+
 // Largest batch of n-point transforms (4096 <= n <= 16384) run in the two-pass
 // split form when out of place.  Measured on MI355X (event time of one call):
 // at n = 16384 the split takes 15-17 us for 1-16 transforms against 17.6-18 us
@@ -416,7 +421,9 @@ int fft_plan_create_ex(int64_t n, int64_t batch, int64_t stride, int64_t dist, i
     p->device = device;
     p->layout = layout;
     p->variant = variant;
-    p->xcd_remap = layout == mi355fft::LAYOUT_COLS && dist == 1;
+    p->xcd_remap = layout == mi355fft::LAYOUT_COLS && dist == 1
+                       ? strip_map(stride * (storage == FFT_STORAGE_FP32 ? 8 : 4))
+                       : mi355fft::XCD_NONE;
     p->tw = tw;
     *plan_out = p;
     return FFT_OK;
@@ -440,7 +447,7 @@ int fft_execute(const fft_plan *plan, const void *in, void *out, hipStream_t str
             const int64_t nb = plan->batch - b0 < 65535 ? plan->batch - b0 : 65535;
             const char *pin = (const char *)in + (size_t)(b0 * plan->dist) * el;
             char *pout = (char *)out + (size_t)(b0 * plan->dist) * el;
-            KArgs a1{n2, n2, 1, n1, 1.0f, 1};
+            KArgs a1{n2, n2, 1, n1, 1.0f, strip_map(n2 * (int64_t)el)};
             a1.out_stride = 1;
             a1.outer = (int)nb;
             a1.outer_in_dist = a1.outer_out_dist = plan->dist;
@@ -448,7 +455,7 @@ int fft_execute(const fft_plan *plan, const void *in, void *out, hipStream_t str
             hipError_t e = launch_fft(n1, plan->v1, mi355fft::LAYOUT_COLS, plan->storage, plan->storage, inv,
                                       mi355fft::EPI_TWIDDLE, pin, pout, plan->tw1, plan->ftab, a1, stream);
             if (e != hipSuccess) return map_hip(e);
-            KArgs a2{n1, n1, 1, 1, plan->scale, 1};
+            KArgs a2{n1, n1, 1, 1, plan->scale, strip_map(n1 * (int64_t)el)};
             a2.outer = (int)nb;
             a2.outer_in_dist = a2.outer_out_dist = plan->dist;
             e = launch_fft(n2, plan->v2, mi355fft::LAYOUT_COLS, plan->storage, plan->storage, inv,
@@ -540,7 +547,7 @@ int sar_form_image_ex(int64_t n_az, int64_t n_rg, int inter_storage, const void 
     if (e != hipSuccess) return map_hip(e);
 
     // pass 2, columns (azimuth): FFT, / n_az * conj(H_a), IFFT -> image
-    const KArgs ac{n_rg, n_rg, 1, 1, (float)(1.0 / (double)n_az), 1};
+    const KArgs ac{n_rg, n_rg, 1, 1, (float)(1.0 / (double)n_az), strip_map(n_rg * 8)};
     e = launch_fft(n_az, vcol, LAYOUT_COLS, inter_storage, FFT_STORAGE_FP32, 0, EPI_MATCHED, mid, out, tw_az, h_az,
                    ac, stream);
     return map_hip(e);
@@ -611,14 +618,14 @@ int sar_rd_form_image(int64_t n_az, int64_t n_rg, int inter_storage, const sar_g
     if (e != hipSuccess) return map_hip(e);
     // 2: azimuth FFT of every range bin (a column), / n_az, written as one row
     //    per range bin (the transposed range-Doppler image)
-    KArgs ab{n_rg, n_rg, 1, n_az, (float)(1.0 / (double)n_az), 1};
+    KArgs ab{n_rg, n_rg, 1, n_az, (float)(1.0 / (double)n_az), strip_map(n_rg * 8)};
     ab.out_stride = 1;
     e = launch_fft(n_az, vcol, LAYOUT_COLS, inter_storage, inter_storage, 0, EPI_SCALE, out, zt, tw_az, nullptr, ab,
                    stream);
     if (e != hipSuccess) return map_hip(e);
     // 3-5: migration correction, azimuth filter and azimuth inverse FFT: reads
     //    rows of the transposed image, writes the columns of the focused image
-    KArgs ac{n_rg, 1, n_az, 1, 1.0f, 1};
+    KArgs ac{n_rg, 1, n_az, 1, 1.0f, strip_map(n_rg * 8)};
     ac.out_stride = n_rg;
     e = launch_fft(n_az, vrcmc, LAYOUT_RCMC, inter_storage, FFT_STORAGE_FP32, 1, EPI_RCMC, zt, out, tw_az,
                    reinterpret_cast<const float2 *>(tables), ac, stream);
