@@ -19,9 +19,9 @@
 // rate, so the bound passes; and the FP16-storage transforms are bound by
 // vector issue, not by memory (their vector kernels issue 53-63 instructions
 // per point), so moving the butterflies to the matrix cores is what could pay.
-// Measured, it does not: with 1 GiB batches from HBM this kernel takes 1.2x
-// (N = 4096) and 1.46x (N = 16384) the time of the vector kernels.  The
-// matrix form removes only 14-16% of the vector instructions per transform,
+// Measured, it does not: with 1 GiB batches from HBM this kernel takes 1.1x
+// (N = 4096) and 1.6x (N = 16384) the time of the vector kernels.  The
+// matrix form removes only 5-16% of the vector instructions per transform,
 // because the operand packing (FP32 -> binary16 fragments), the twiddles and
 // the Stockham moves through LDS stay on the vector units; the matrix cores
 // are busy about a fifth of the time.  It is kept as an opt-in plan flag.
