@@ -717,20 +717,45 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
             transform<K, INV, EPI, true>(v, t, c, tw, spec, a.scale, lds);
         }
         if constexpr (EPI == EPI_TWIDDLE) {
-            // four-step: point k1 = t + T*i of column n2 times W_N^(n2 k1)
-            // = W_N^(n2 t) * W_N^(n2 T i).  Each factor is looked up exactly
-            // (W^m = lo[m mod S] * hi[m div S], n2 k1 < N): the first once per
-            // thread, the second shared by the lanes of a column (a broadcast
-            // read), instead of a scattered pair of reads per point.
+            // four-step: point k1 = t + T*i of column n2 times W_N^(n2 k1).
+            // Four factors are looked up exactly (W^m = lo[m mod S] *
+            // hi[m div S], m < N): W^(n2 t), W^(n2 T), W^(4 n2 T) and
+            // W^(16 n2 T).  With i = i0 + 4 g, the point's factor is
+            // c[i0] * H[g], where c[i0] = W^(n2 t) W^(n2 T i0) and H[g] is
+            // the product of the powers of the other two for the base-4
+            // digits of g: eight table reads per thread instead of two per
+            // point, at most six products deep.
+            static_assert(K::P % 4 == 0 && K::P <= 32, "four-step columns hold 4 to 32 points per thread");
             const float2 *lo = spec, *hi = spec + (1 << a.aux);
             const int mask = (1 << a.aux) - 1;
             const int n2 = (int)(blk * K::C) + (valid ? c : 0);
-            const int m0 = n2 * t;
-            const float2 base = cmul(lo[m0 & mask], hi[m0 >> a.aux]);
-            static_for<0, K::P>([&](auto ic) {
-                const int m = n2 * (K::T * decltype(ic)::value);
-                const float2 w = cmul(base, cmul(lo[m & mask], hi[m >> a.aux]));
-                v[ic] = INV ? cmulc(v[ic], w) : cmul(v[ic], w);
+            auto look = [&](int m) { return cmul(lo[m & mask], hi[m >> a.aux]); };
+            float2 cf[4];
+            cf[0] = look(n2 * t);
+            const float2 w1 = look(n2 * K::T);
+            const float2 w2 = cmul(w1, w1);
+            cf[1] = cmul(cf[0], w1);
+            cf[2] = cmul(cf[0], w2);
+            cf[3] = cmul(cf[2], w1);
+            constexpr int NG = K::P / 4;
+            float2 e1[3], e2 = make_float2(1.0f, 0.0f);
+            if constexpr (NG > 1) {
+                e1[0] = look(n2 * K::T * 4);
+                e1[1] = cmul(e1[0], e1[0]);
+                e1[2] = cmul(e1[1], e1[0]);
+            }
+            if constexpr (NG > 4) e2 = look(n2 * K::T * 16);
+            static_for<0, NG>([&](auto gc) {
+                constexpr int g = decltype(gc)::value, g0 = g % 4, g1 = g / 4;
+                float2 h = make_float2(1.0f, 0.0f);
+                if constexpr (g0 != 0 && g1 != 0) h = cmul(e1[g0 - 1], e2);
+                if constexpr (g0 != 0 && g1 == 0) h = e1[g0 - 1];
+                if constexpr (g0 == 0 && g1 != 0) h = e2;
+                static_for<0, 4>([&](auto jc) {
+                    constexpr int i = 4 * g + decltype(jc)::value;
+                    const float2 w = g == 0 ? cf[decltype(jc)::value] : cmul(cf[decltype(jc)::value], h);
+                    v[i] = INV ? cmulc(v[i], w) : cmul(v[i], w);
+                });
             });
         }
         if constexpr (EPI == EPI_RCMC || EPI == EPI_SCALE || EPI == EPI_TWIDDLE) {
