@@ -703,10 +703,14 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
     const int t = K::COLS ? (tid >> K::LOG_C) : (tid & (K::T - 1));
     float2 v[K::P];
     if constexpr (!K::PERSIST) {
-        // strips per 128-byte line, from the narrower of the two sides' pieces
+        // strips per 128-byte line, from the narrower of the two sides' pieces;
+        // the migration pass keeps groups of at least 8 strips on an XCD, since
+        // neighbouring strips also read overlapping windows of rows (FETCH_SIZE
+        // 1.3x its input instead of 2.1x with groups of 2)
         constexpr int PIECE = K::C * (Store<IN_ST>::BYTES < Store<OUT_ST>::BYTES ? Store<IN_ST>::BYTES
                                                                                 : Store<OUT_ST>::BYTES);
-        constexpr int GROUP = PIECE >= 128 ? 1 : 128 / PIECE;
+        constexpr int LINE_GROUP = PIECE >= 128 ? 1 : 128 / PIECE;
+        constexpr int GROUP = EPI == EPI_RCMC && LINE_GROUP < 8 ? 8 : LINE_GROUP;
         const long long blk = logical_block<GROUP>(a.xcd_remap);
         const bool valid = blk * K::C + c < a.batch;
         if constexpr (EPI == EPI_RCMC) {
