@@ -155,7 +155,7 @@ struct Configs<16384> {
     using RowsHalf = KList<KCfg<16384, 32, 1, false, XCHG_HALF, 1, false, Radices<32, 16, 32>>,
                            KCfg<16384, 32, 1, false, XCHG_HALF, 1, false, Radices<16, 16, 16, 4>>,
                            KCfg<16384, 16, 1, false, XCHG_HALF, 1, false, Radices<16, 16, 16, 4>>>;
-    static constexpr int kRowMatched = 1, kColMatched = 1;
+    static constexpr int kRowMatched = 4, kColMatched = 1;
 };
 
 // Small batches: a batch that gives the default row shape (several
