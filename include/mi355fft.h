@@ -72,9 +72,12 @@ typedef struct fft_plan fft_plan; /* opaque; immutable once created */
  *            FFT_EUNSUPPORTED.  Up to 16384 every transform is one pass
  *            (read once, written once).  Longer transforms use the two-pass
  *            four-step form (Section VI: the transform no longer fits on
- *            chip): n = n1 * n2 with n2 = 2^floor(log2(n) / 2); they require
- *            stride == 1 (else FFT_EUNSUPPORTED) and out-of-place execution,
- *            and use `out` for the intermediate.  Batches of at most 16
+ *            chip): n = n1 * n2 with n2 = 2^floor(log2(n) / 2); beyond 2^22
+ *            a third pass splits n2 again (n = n1 * na * nb, no factor above
+ *            1024, so that every pass reads and writes wide pieces of each
+ *            row).  They require stride == 1 (else FFT_EUNSUPPORTED) and
+ *            out-of-place execution, and use `out` for the intermediate; the
+ *            input is not modified.  Batches of at most 16
  *            contiguous 16384-point transforms executed out of place take the
  *            same split (128 x 128) to spread each transform over more
  *            workgroups (Section VI's advice for small batches); in place
@@ -97,9 +100,10 @@ typedef struct fft_plan fft_plan; /* opaque; immutable once created */
  * Creates (once per device and size, shared by all plans, kept until the
  * process ends) a device table of the n twiddle factors exp(-2 pi i m / n),
  * computed in double precision on the host and rounded once to FP32; for
- * four-step lengths, the tables of n1 and n2 and a two-level table of the
- * factors exp(-2 pi i m / n) (about 2 sqrt(n) entries, W^m formed as the
- * product of two entries).  Uses the current HIP device; the plan must be
+ * four-step lengths, the tables of n1 and n2 (n1, na and nb) and two-level
+ * tables of the factors exp(-2 pi i m / n) (and, with three passes, of
+ * exp(-2 pi i m / (na nb))), each about 2 sqrt(n) entries, W^m formed as the
+ * product of two entries.  Uses the current HIP device; the plan must be
  * executed on that device.
  * Returns FFT_OK, FFT_EINVAL, FFT_EUNSUPPORTED, FFT_ENOMEM or FFT_EHIP.
  */

@@ -205,7 +205,9 @@ hipError_t with_variant(int idx, KList<K, Ks...>, F &&f) {
 //   scaled:     columns, forward, input storage == output storage (the azimuth
 //               FFT of the full range-Doppler chain);
 //   twiddled:   columns, either direction, input storage == output storage,
-//               written as rows (first pass of a four-step transform);
+//               written as rows (first pass of a four-step transform), or
+//               written in place with the factor keyed by the second grid
+//               axis (middle pass of a three-pass transform);
 //   RCMC:       the Rcmc list (row-mapped, several transforms per workgroup),
 //               inverse, read FP32 or FP16, write FP32 columns (migration
 //               correction, azimuth filter and azimuth inverse FFT).
@@ -237,6 +239,18 @@ hipError_t dispatch_cfg_full(int in_st, int out_st, int inv, int epi, const void
                            : launch_one<K, 0, 0, false, EPI_TWIDDLE>(in, out, tw, spec, a, s);
             return inv ? launch_one<K, 1, 1, true, EPI_TWIDDLE>(in, out, tw, spec, a, s)
                        : launch_one<K, 1, 1, false, EPI_TWIDDLE>(in, out, tw, spec, a, s);
+        } else {
+            return hipErrorInvalidValue;
+        }
+    }
+    if (epi == EPI_TWIDDLE_Y) {
+        if constexpr (K::COLS && !K::PERSIST) {
+            if (in_st != out_st) return hipErrorInvalidValue;
+            if (in_st == 0)
+                return inv ? launch_one<K, 0, 0, true, EPI_TWIDDLE_Y>(in, out, tw, spec, a, s)
+                           : launch_one<K, 0, 0, false, EPI_TWIDDLE_Y>(in, out, tw, spec, a, s);
+            return inv ? launch_one<K, 1, 1, true, EPI_TWIDDLE_Y>(in, out, tw, spec, a, s)
+                       : launch_one<K, 1, 1, false, EPI_TWIDDLE_Y>(in, out, tw, spec, a, s);
         } else {
             return hipErrorInvalidValue;
         }

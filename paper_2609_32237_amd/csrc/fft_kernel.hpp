@@ -621,7 +621,20 @@ __device__ __forceinline__ void store_remapped(float2 (&v)[K::P], void *__restri
             v[ic] = make_float2(re[ic], lds[rbase + lds_offset<K>(T * decltype(ic)::value)]);
         });
     }
-    if (blk * K::C + c2 < a.batch) store_points<K, ST, false>(v, out, blk, c2, t2, a);
+    const long long m = blk * K::C + c2;
+    if (m >= a.batch) return;
+    if (a.perm_b == 0) {
+        store_points<K, ST, false>(v, out, blk, c2, t2, a);
+    } else {
+        // permuted rows: each lands in its own row, so address by pointer
+        const long long row = ((m & ((1LL << a.perm_b) - 1)) << a.perm_a) | (m >> a.perm_b);
+        using E = typename Store<ST>::T;
+        E *dst = reinterpret_cast<E *>(out) + row * a.out_dist;
+        static_for<0, P>([&](auto ic) {
+            const long long pos = t2 + T * decltype(ic)::value;
+            Store<ST>::template store<false>(dst + pos * a.out_stride, v[ic]);
+        });
+    }
 }
 
 // The whole on-chip computation of one transform (first exchange of the
@@ -720,7 +733,7 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
             load_points<K, IN_ST>(v, in, blk, c, t, valid, a);
             transform<K, INV, EPI, true>(v, t, c, tw, spec, a.scale, lds);
         }
-        if constexpr (EPI == EPI_TWIDDLE) {
+        if constexpr (EPI == EPI_TWIDDLE || EPI == EPI_TWIDDLE_Y) {
             // four-step: point k1 = t + T*i of column n2 times W_N^(n2 k1).
             // Four factors are looked up exactly (W^m = lo[m mod S] *
             // hi[m div S], m < N): W^(n2 t), W^(n2 T), W^(4 n2 T) and
@@ -732,7 +745,8 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
             static_assert(K::P % 4 == 0 && K::P <= 32, "four-step columns hold 4 to 32 points per thread");
             const float2 *lo = spec, *hi = spec + (1 << a.aux);
             const int mask = (1 << a.aux) - 1;
-            const int n2 = (int)(blk * K::C) + (valid ? c : 0);
+            // the column's index, or for EPI_TWIDDLE_Y the problem's
+            const int n2 = EPI == EPI_TWIDDLE_Y ? (int)blockIdx.y : (int)(blk * K::C) + (valid ? c : 0);
             auto look = [&](int m) { return cmul(lo[m & mask], hi[m >> a.aux]); };
             float2 cf[4];
             cf[0] = look(n2 * t);

@@ -24,6 +24,9 @@ enum { LAYOUT_ROWS = 0, LAYOUT_COLS = 1, LAYOUT_RCMC = 2, LAYOUT_ROWS_HALF = 3 }
 //                azimuth filter), the inverse transform runs, and the result
 //                is written as columns; `spec` points to the range-Doppler
 //                tables below.
+//   EPI_TWIDDLE_Y  middle pass of a three-pass transform: plain column strips,
+//                output point k of problem blockIdx.y times W^(blockIdx.y k)
+//                (the same two-level tables as EPI_TWIDDLE);
 //   EPI_TWIDDLE  first pass of a four-step transform of length N = N1 * N2:
 //                the column FFT of length N1, point k1 of column n2 times
 //                W_N^(n2 k1) (conjugate for the inverse), written as rows;
@@ -31,7 +34,7 @@ enum { LAYOUT_ROWS = 0, LAYOUT_COLS = 1, LAYOUT_RCMC = 2, LAYOUT_ROWS_HALF = 3 }
 //                m < N / S, with S = 2^aux.
 // Block -> strip maps of column kernels over the 8 XCDs (logical_block).
 enum { XCD_NONE = 0, XCD_CONTIG = 1, XCD_GROUPS = 2 };
-enum { EPI_NONE = 0, EPI_MATCHED = 1, EPI_SCALE = 2, EPI_RCMC = 3, EPI_TWIDDLE = 4 };
+enum { EPI_NONE = 0, EPI_MATCHED = 1, EPI_SCALE = 2, EPI_RCMC = 3, EPI_TWIDDLE = 4, EPI_TWIDDLE_Y = 5 };
 
 // Range-Doppler tables, one device block in this order (byte offsets from
 // rd_tables_layout; the interpolator rows are copied in from `interp_src`):
@@ -70,7 +73,10 @@ struct KArgs {
     long long outer_in_dist;   // elements between the problems of blockIdx.y (input)
     long long outer_out_dist;  // elements between the problems of blockIdx.y (output)
     int outer;                 // problems along blockIdx.y (0 or 1: one)
-    int aux;                   // EPI_TWIDDLE: log2 of the low twiddle table's length
+    int aux;                   // EPI_TWIDDLE(_Y): log2 of the low twiddle table's length
+    // EPI_TWIDDLE with a row permutation: transform m of the batch is written
+    // as row ((m mod 2^perm_b) << perm_a) | (m >> perm_b) (0, 0: row m)
+    int perm_a, perm_b;
 };
 
 // Fills the addressing fields of `a` for workgroups of `c` transforms of `n`

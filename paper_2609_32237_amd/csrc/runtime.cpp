@@ -31,12 +31,18 @@ struct fft_plan {
     int64_t n1, n2;
     int log2s, v1, v2;
     const float2 *tw1, *tw2, *ftab;
+    // three passes (n > 2^24): n2 = na * nb, pass 2 split into a pass of
+    // na-point and a pass of nb-point columns (0: two passes)
+    int64_t na, nb;
+    int log2s2, va, vb;
+    const float2 *twa, *twb, *ftab2;
 };
 
 namespace {
 
 constexpr int64_t kMinN = 1024, kMaxN = 16384;      // single-pass transforms
-constexpr int64_t kMaxFourStep = int64_t(1) << 28;  // two passes: n1 * n2, each <= 16384
+constexpr int64_t kMaxFourStep = int64_t(1) << 28;  // longest transform
+constexpr int64_t kMaxTwoPass = int64_t(1) << 22;   // two passes up to here, then three
 constexpr int64_t kMaxIndex = int64_t(1) << 40;  // largest element index accepted
 
 bool is_pow2(int64_t n) { return n > 0 && (n & (n - 1)) == 0; }
@@ -374,13 +380,25 @@ int fft_plan_create_ex(int64_t n, int64_t batch, int64_t stride, int64_t dist, i
     if (batch > (int64_t)0x7fffffff) return FFT_EUNSUPPORTED;  // grid size limit
     const int layout = half_x ? mi355fft::LAYOUT_ROWS_HALF
                               : stride == 1 ? mi355fft::LAYOUT_ROWS : mi355fft::LAYOUT_COLS;
-    // four-step split: n2 = 2^floor(log2 n / 2), n1 = n / n2 (both in [128, 16384])
+    // four-step split: n2 = 2^floor(log2 n / 2), n1 = n / n2 (both in [128, 2048]).
+    // Beyond 2^22 a two-factor split needs columns of 4096 points or more,
+    // whose strips are 8 columns or fewer wide (64-, 16- or 8-byte pieces of
+    // each row); three passes of at most 1024-point columns move the data
+    // once more but faster: n1 = 2^floor(log2 n / 3) and n2 = n / n1 =
+    // na * nb, na = 2^floor(log2 n2 / 2).  Measured on MI355X (1 GiB,
+    // 16 B/pt): 2^23 1.74 against 1.59 TB/s, 2^24 1.81 against 1.69,
+    // 2^28 1.25 against 0.47; at 2^20-2^22 two passes stay ahead.
     const bool split = four_step || may_split;
-    const int64_t n2 = split ? int64_t(1) << (ilog2(n) / 2) : 0, n1 = split ? n / n2 : 0;
+    const bool three = four_step && n > kMaxTwoPass;
+    const int64_t n2 = !split ? 0 : three ? n >> (ilog2(n) / 3) : int64_t(1) << (ilog2(n) / 2);
+    const int64_t n1 = split ? n / n2 : 0;
+    const int64_t na = three ? int64_t(1) << (ilog2(n2) / 2) : 0, nb = three ? n2 / na : 0;
     const int variant = four_step ? -1 : chosen_variant(n, layout);
     const int v1 = split ? chosen_variant(n1, mi355fft::LAYOUT_COLS) : -1;
-    const int v2 = split ? chosen_variant(n2, mi355fft::LAYOUT_COLS) : -1;
-    if (variant == -2 || v1 == -2 || v2 == -2) return FFT_EINVAL;
+    const int v2 = split && !three ? chosen_variant(n2, mi355fft::LAYOUT_COLS) : -1;
+    const int va = three ? chosen_variant(na, mi355fft::LAYOUT_COLS) : -1;
+    const int vb = three ? chosen_variant(nb, mi355fft::LAYOUT_COLS) : -1;
+    if (variant == -2 || v1 == -2 || v2 == -2 || va == -2 || vb == -2) return FFT_EINVAL;
     if (four_step && batch > (int64_t)0x7fffffff) return FFT_EUNSUPPORTED;
     if (fail_alloc_hook()) return FFT_ENOMEM;  // test hook: device allocation fails
 
@@ -388,12 +406,19 @@ int fft_plan_create_ex(int64_t n, int64_t batch, int64_t stride, int64_t dist, i
     hipError_t e = hipGetDevice(&device);
     if (e != hipSuccess) return map_hip(e);
     const float2 *tw = nullptr, *tw1 = nullptr, *tw2 = nullptr, *ftab = nullptr;
+    const float2 *twa = nullptr, *twb = nullptr, *ftab2 = nullptr;
     const int log2s = split ? (ilog2(n) + 1) / 2 : 0;
+    const int log2s2 = three ? (ilog2(n2) + 1) / 2 : 0;
     int rc = FFT_OK;
     if (split) {
         rc = get_twiddles(device, n1, &tw1);
-        if (rc == FFT_OK) rc = get_twiddles(device, n2, &tw2);
+        if (rc == FFT_OK && !three) rc = get_twiddles(device, n2, &tw2);
         if (rc == FFT_OK) rc = get_fourstep_table(device, n, log2s, &ftab);
+    }
+    if (three) {
+        if (rc == FFT_OK) rc = get_twiddles(device, na, &twa);
+        if (rc == FFT_OK) rc = get_twiddles(device, nb, &twb);
+        if (rc == FFT_OK) rc = get_fourstep_table(device, n2, log2s2, &ftab2);
     }
     if (rc == FFT_OK && !four_step) rc = get_twiddles(device, n, &tw);
     const void *amat = nullptr;
@@ -412,6 +437,14 @@ int fft_plan_create_ex(int64_t n, int64_t batch, int64_t stride, int64_t dist, i
     p->tw1 = tw1;
     p->tw2 = tw2;
     p->ftab = ftab;
+    p->na = na;
+    p->nb = nb;
+    p->log2s2 = log2s2;
+    p->va = va;
+    p->vb = vb;
+    p->twa = twa;
+    p->twb = twb;
+    p->ftab2 = ftab2;
     p->n = n;
     p->batch = batch;
     p->stride = stride;
@@ -429,6 +462,55 @@ int fft_plan_create_ex(int64_t n, int64_t batch, int64_t stride, int64_t dist, i
     return FFT_OK;
 }
 
+// Three passes for n = n1 * na * nb (x viewed as n1 x n2, n2 = na * nb, j =
+// n2 j1 + j2, j2 = nb ja + jb):
+//   pass 1  the n2 columns of length n1, times W_n^(j2 k1), column j2 written
+//           as row na (j2 mod nb) + (j2 div nb) of `out`: each problem's nb
+//           groups of na rows then sit together;
+//   pass 2  in place, for each jb, the n1 columns of length na of its group
+//           of rows, output ka times W_n2^(jb ka);
+//   pass 3  in place, for each ka, the n1 columns of length nb through rows
+//           ka, ka + na, ... : row ka + na kb then holds X[k1 + n1 (ka + na kb)],
+//           the natural order.
+static int execute_three_pass(const fft_plan *plan, const void *in, void *out, int inv, hipStream_t stream) {
+    const size_t el = plan->storage == FFT_STORAGE_FP32 ? 8 : 4;
+    const int64_t n1 = plan->n1, n2 = plan->n2, na = plan->na, nb = plan->nb;
+    for (int64_t b0 = 0; b0 < plan->batch; b0 += 65535) {
+        const int64_t nbat = plan->batch - b0 < 65535 ? plan->batch - b0 : 65535;
+        const char *pin = (const char *)in + (size_t)(b0 * plan->dist) * el;
+        char *pout = (char *)out + (size_t)(b0 * plan->dist) * el;
+        KArgs a1{n2, n2, 1, n1, 1.0f, strip_map(n2 * (int64_t)el)};
+        a1.out_stride = 1;
+        a1.outer = (int)nbat;
+        a1.outer_in_dist = a1.outer_out_dist = plan->dist;
+        a1.aux = plan->log2s;
+        a1.perm_a = ilog2(na);
+        a1.perm_b = ilog2(nb);
+        hipError_t e = launch_fft(n1, plan->v1, mi355fft::LAYOUT_COLS, plan->storage, plan->storage, inv,
+                                  mi355fft::EPI_TWIDDLE, pin, pout, plan->tw1, plan->ftab, a1, stream);
+        if (e != hipSuccess) return map_hip(e);
+    }
+    // passes 2 and 3 use the grid's second axis for the groups: one launch
+    // per problem
+    for (int64_t b = 0; b < plan->batch; ++b) {
+        char *p = (char *)out + (size_t)(b * plan->dist) * el;
+        KArgs a2{n1, n1, 1, 1, 1.0f, strip_map(n1 * (int64_t)el)};
+        a2.outer = (int)nb;
+        a2.outer_in_dist = a2.outer_out_dist = na * n1;
+        a2.aux = plan->log2s2;
+        hipError_t e = launch_fft(na, plan->va, mi355fft::LAYOUT_COLS, plan->storage, plan->storage, inv,
+                                  mi355fft::EPI_TWIDDLE_Y, p, p, plan->twa, plan->ftab2, a2, stream);
+        if (e != hipSuccess) return map_hip(e);
+        KArgs a3{n1, na * n1, 1, 1, plan->scale, strip_map(na * n1 * (int64_t)el)};
+        a3.outer = (int)na;
+        a3.outer_in_dist = a3.outer_out_dist = n1;
+        e = launch_fft(nb, plan->vb, mi355fft::LAYOUT_COLS, plan->storage, plan->storage, inv, mi355fft::EPI_NONE,
+                       p, p, plan->twb, nullptr, a3, stream);
+        if (e != hipSuccess) return map_hip(e);
+    }
+    return FFT_OK;
+}
+
 int fft_execute(const fft_plan *plan, const void *in, void *out, hipStream_t stream) {
     if (!plan || !in || !out) return FFT_EINVAL;
     const size_t el = plan->storage == FFT_STORAGE_FP32 ? 8 : 4;
@@ -443,6 +525,7 @@ int fft_execute(const fft_plan *plan, const void *in, void *out, hipStream_t str
         if (in == out) return FFT_EINVAL;
         const int inv = plan->dir == FFT_INVERSE;
         const int64_t n1 = plan->n1, n2 = plan->n2;
+        if (plan->na) return execute_three_pass(plan, in, out, inv, stream);
         for (int64_t b0 = 0; b0 < plan->batch; b0 += 65535) {
             const int64_t nb = plan->batch - b0 < 65535 ? plan->batch - b0 : 65535;
             const char *pin = (const char *)in + (size_t)(b0 * plan->dist) * el;

@@ -82,6 +82,34 @@ def test_2_pow_24_matches_oracle(lib):
     assert err.max() < 1e-5, err
 
 
+@pytest.mark.parametrize("storage", [0, 1])
+def test_three_pass_lengths_match_oracle(lib, storage):
+    """Beyond 2^24 the transform takes three passes (n1 x na x nb, columns of
+    at most 1024 points); 2^25 = 256 x 256 x 512, two transforms in both
+    directions, and a scaled inverse."""
+    import torch
+
+    n, batch = 1 << 25, 2
+    st = "fp32" if storage == 0 else "fp16"
+    x = workloads.uniform_complex(batch, n, 925, st)
+    for direction in (-1, 1):
+        log(f"three-pass n=2^25 {st} dir={direction}")
+        y = widen(run(lib, x, n, batch, n, storage, direction))
+        err = rel_rows(y, oracle.fft(x, direction))
+        assert err.max() < TOL[storage], (storage, direction, err.max())
+    if storage == 0:
+        xd = to_dev(x)
+        yd = torch.empty_like(xd)
+        p = lib.fft_plan_create_ex(n, batch, 1, n, 0, 1, 25, 0)
+        try:
+            lib.fft_execute(p, xd.data_ptr(), yd.data_ptr(), torch.cuda.current_stream().cuda_stream)
+            torch.cuda.synchronize()
+        finally:
+            lib.fft_plan_destroy(p)
+        err = rel_rows(widen(to_host(yd)), oracle.fft(x, 1) / n)
+        assert err.max() < TOL[0], err.max()
+
+
 def test_largest_length_closed_forms(lib):
     """n = 2^28 (2 GiB per FP32 transform): an impulse at n0 transforms to
     exp(-2 pi i k n0 / n); sampled outputs against that closed form in double,
