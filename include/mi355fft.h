@@ -92,7 +92,11 @@ typedef struct fft_plan fft_plan; /* opaque; immutable once created */
  *            (stride >= (batch-1)*dist + 1), else FFT_EINVAL.
  *            stride == 1 selects the contiguous-row kernels; stride > 1 the
  *            strided-column kernels (columns of a row-major matrix are
- *            stride = row length, dist = 1).
+ *            stride = row length, dist = 1).  Columns of 8192 or 16384
+ *            points with dist == 1 executed out of place run as two passes
+ *            of 128 x 64 or 128 x 128 points (the four-step form along the
+ *            columns), using `out` for the intermediate; in place they stay
+ *            single-pass.
  *   storage  FFT_STORAGE_FP32 or FFT_STORAGE_FP16 (input and output alike).
  *   dir      FFT_FORWARD or FFT_INVERSE.
  *   plan_out receives the plan; untouched on error.

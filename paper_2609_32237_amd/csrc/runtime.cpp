@@ -36,6 +36,8 @@ struct fft_plan {
     int64_t na, nb;
     int log2s2, va, vb;
     const float2 *twa, *twb, *ftab2;
+    // long interleaved columns as two passes of short columns (out of place)
+    bool colsplit;
 };
 
 namespace {
@@ -315,6 +317,18 @@ int64_t split_batch(int64_t n) {
     return (*end == '\0' && v > 0) ? v : 0;
 }
 
+// Long strided columns (8192 or 16384 points, interleaved: dist 1) executed
+// out of place run as two passes of short columns: a 8192- or 16384-point
+// column kernel holds one or two columns per workgroup, so it reads 8- or
+// 16-byte pieces of each row, while 64- and 128-point column kernels hold
+// 32-64 columns.  A forced column shape (MI355FFT_COL_VARIANT) keeps the
+// single pass.
+bool column_split(int64_t n, int64_t dist, int storage_layout_cols) {
+    const char *cv = std::getenv("MI355FFT_COL_VARIANT");
+    if (cv && cv[0]) return false;
+    return storage_layout_cols && dist == 1 && (n == 8192 || n == 16384);
+}
+
 bool overlaps(const void *a, size_t na, const void *b, size_t nb) {
     const char *pa = (const char *)a, *pb = (const char *)b;
     return pa < pb + nb && pb < pa + na;
@@ -388,9 +402,11 @@ int fft_plan_create_ex(int64_t n, int64_t batch, int64_t stride, int64_t dist, i
     // na * nb, na = 2^floor(log2 n2 / 2).  Measured on MI355X (1 GiB,
     // 16 B/pt): 2^23 1.74 against 1.59 TB/s, 2^24 1.81 against 1.69,
     // 2^28 1.25 against 0.47; at 2^20-2^22 two passes stay ahead.
-    const bool split = four_step || may_split;
+    const bool colsplit = !half_x && !mfma && stride > 1 && column_split(n, dist, 1);
+    const bool split = four_step || may_split || colsplit;
     const bool three = four_step && n > kMaxTwoPass;
-    const int64_t n2 = !split ? 0 : three ? n >> (ilog2(n) / 3) : int64_t(1) << (ilog2(n) / 2);
+    // long columns: n1 = 128, n2 = 64 or 128
+    const int64_t n2 = !split ? 0 : three ? n >> (ilog2(n) / 3) : colsplit ? n / 128 : int64_t(1) << (ilog2(n) / 2);
     const int64_t n1 = split ? n / n2 : 0;
     const int64_t na = three ? int64_t(1) << (ilog2(n2) / 2) : 0, nb = three ? n2 / na : 0;
     const int variant = four_step ? -1 : chosen_variant(n, layout);
@@ -437,6 +453,7 @@ int fft_plan_create_ex(int64_t n, int64_t batch, int64_t stride, int64_t dist, i
     p->tw1 = tw1;
     p->tw2 = tw2;
     p->ftab = ftab;
+    p->colsplit = colsplit;
     p->na = na;
     p->nb = nb;
     p->log2s2 = log2s2;
@@ -511,11 +528,39 @@ static int execute_three_pass(const fft_plan *plan, const void *in, void *out, i
     return FFT_OK;
 }
 
+// Columns of length n = n1 * n2 (point j of column c at j S + c, S the
+// stride), j = n2 j1 + j2:
+//   pass 1  for each j2 (the grid's second axis), the columns of length n1
+//           through rows n2 j1 + j2, output k1 times W_n^(j2 k1), written to
+//           rows j2 n1 + k1 of `out`;
+//   pass 2  in place, for each k1, the columns of length n2 through rows
+//           j2 n1 + k1: row k1 + n1 k2 then holds X[k1 + n1 k2].
+static int execute_column_split(const fft_plan *plan, const void *in, void *out, int inv, hipStream_t stream) {
+    const int64_t n1 = plan->n1, n2 = plan->n2, s = plan->stride;
+    const size_t el = plan->storage == FFT_STORAGE_FP32 ? 8 : 4;
+    KArgs a1{plan->batch, n2 * s, 1, 1, 1.0f, strip_map(n2 * s * (int64_t)el)};
+    a1.out_stride = s;
+    a1.outer = (int)n2;
+    a1.outer_in_dist = s;
+    a1.outer_out_dist = n1 * s;
+    a1.aux = plan->log2s;
+    hipError_t e = launch_fft(n1, plan->v1, mi355fft::LAYOUT_COLS, plan->storage, plan->storage, inv,
+                              mi355fft::EPI_TWIDDLE_Y, in, out, plan->tw1, plan->ftab, a1, stream);
+    if (e != hipSuccess) return map_hip(e);
+    KArgs a2{plan->batch, n1 * s, 1, 1, plan->scale, strip_map(n1 * s * (int64_t)el)};
+    a2.outer = (int)n1;
+    a2.outer_in_dist = a2.outer_out_dist = s;
+    e = launch_fft(n2, plan->v2, mi355fft::LAYOUT_COLS, plan->storage, plan->storage, inv, mi355fft::EPI_NONE, out,
+                   out, plan->tw2, nullptr, a2, stream);
+    return map_hip(e);
+}
+
 int fft_execute(const fft_plan *plan, const void *in, void *out, hipStream_t stream) {
     if (!plan || !in || !out) return FFT_EINVAL;
     const size_t el = plan->storage == FFT_STORAGE_FP32 ? 8 : 4;
     if (!aligned(in, el) || !aligned(out, el)) return FFT_EALIGN;
-    if (plan->n1 && (plan->n > kMaxN || in != out)) {
+    if (plan->colsplit && in != out) return execute_column_split(plan, in, out, plan->dir == FFT_INVERSE, stream);
+    if (plan->n1 && !plan->colsplit && (plan->n > kMaxN || in != out)) {
         // four-step (Section VI's two-pass transform for lengths beyond the
         // chip): pass 1 transforms the n2 columns of length n1 of each
         // problem viewed as an n1 x n2 matrix, multiplies point k1 of column
