@@ -194,7 +194,11 @@ size_t sar_workspace_bytes(int64_t n_az, int64_t n_rg, int inter_storage);
  *                   raw or the workspace.
  *   workspace       sar_workspace_bytes(n_az, n_rg, inter_storage) bytes,
  *                   256-byte aligned; contents on entry are ignored.
- *   stream          HIP stream; three kernels are launched on it in order.
+ *   stream          HIP stream; three kernels are launched on it in order
+ *                   (five for n_az of 8192 or 16384 with FP32 intermediates,
+ *                   whose azimuth pass runs as three passes of short columns;
+ *                   `out` then also holds the range-compressed image between
+ *                   the passes).
  *
  * Computes, with H_r = FFT(range_ref) and H_a = FFT(az_ref):
  *   y[a, :]   = IFFT( FFT(raw[a, :]) * conj(H_r) ) / n_rg      (pass 1, rows)

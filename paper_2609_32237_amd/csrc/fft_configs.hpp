@@ -255,6 +255,14 @@ hipError_t dispatch_cfg_full(int in_st, int out_st, int inv, int epi, const void
             return hipErrorInvalidValue;
         }
     }
+    if (epi == EPI_MATCHED_Y) {
+        if constexpr (K::COLS && !K::PERSIST) {
+            if (inv || in_st != 0 || out_st != 0) return hipErrorInvalidValue;
+            return launch_one<K, 0, 0, false, EPI_MATCHED_Y>(in, out, tw, spec, a, s);
+        } else {
+            return hipErrorInvalidValue;
+        }
+    }
     if (epi == EPI_RCMC) return hipErrorInvalidValue;  // only through dispatch_rcmc
     if (epi != EPI_MATCHED || inv) return hipErrorInvalidValue;
     if constexpr (!K::COLS) {
@@ -310,7 +318,7 @@ hipError_t dispatch(int variant, int layout, int in_st, int out_st, int inv, int
         }
     }
     const int half = (in_st | out_st) != 0;  // any FP16 storage involved
-    const bool mf = epi == EPI_MATCHED;
+    const bool mf = epi == EPI_MATCHED || epi == EPI_MATCHED_Y;
     if (layout == LAYOUT_ROWS) {
         int v = variant >= 0 ? variant : mf ? Configs<N>::kRowMatched : Configs<N>::kRowDefault[half];
         if (variant < 0 && !mf && epi == EPI_NONE && a.batch < SmallRows<N>::below) v = SmallRows<N>::variant;

@@ -641,8 +641,9 @@ __device__ __forceinline__ void store_remapped(float2 (&v)[K::P], void *__restri
 // kernel may skip its leading barrier).
 template <class K, bool INV, int EPI, bool FIRST_X>
 __device__ __forceinline__ void transform(float2 (&v)[K::P], int t, int c, const float2 *__restrict__ tw,
-                                          const float2 *__restrict__ spec, float scale, float *lds) {
-    constexpr bool MF = EPI == EPI_MATCHED;
+                                          const float2 *__restrict__ spec, float scale, float *lds,
+                                          int spec_off = 0, int spec_shift = 0) {
+    constexpr bool MF = EPI == EPI_MATCHED || EPI == EPI_MATCHED_Y;
     run_fft<K, INV, FIRST_X>(typename K::Rad{}, v, t, c, tw, lds);
     if constexpr (MF) {
         // X[k] * conj(H[k]) * scale, k = t + T*i, then the inverse transform.
@@ -655,7 +656,7 @@ __device__ __forceinline__ void transform(float2 (&v)[K::P], int t, int c, const
         static_for<0, K::P / HC>([&](auto jc) {
             static_for<0, HC>([&](auto ec) {
                 constexpr int i = decltype(jc)::value * HC + decltype(ec)::value;
-                const float2 y = cmulc(v[i], spec[t + K::T * i]);
+                const float2 y = cmulc(v[i], spec[spec_off + ((t + K::T * i) << spec_shift)]);
                 v[i] = make_float2(y.x * scale, y.y * scale);
             });
             __builtin_amdgcn_sched_barrier(0);
@@ -731,9 +732,13 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
             transform<K, INV, EPI_NONE, true>(v, t, c, tw, spec, a.scale, lds);
         } else {
             load_points<K, IN_ST>(v, in, blk, c, t, valid, a);
-            transform<K, INV, EPI, true>(v, t, c, tw, spec, a.scale, lds);
+            if constexpr (EPI == EPI_MATCHED_Y) {
+                transform<K, INV, EPI, true>(v, t, c, tw, spec, a.scale, lds, (int)blockIdx.y, a.spec_shift);
+            } else {
+                transform<K, INV, EPI, true>(v, t, c, tw, spec, a.scale, lds);
+            }
         }
-        if constexpr (EPI == EPI_TWIDDLE || EPI == EPI_TWIDDLE_Y) {
+        if constexpr (EPI == EPI_TWIDDLE || EPI == EPI_TWIDDLE_Y || EPI == EPI_MATCHED_Y) {
             // four-step: point k1 = t + T*i of column n2 times W_N^(n2 k1).
             // Four factors are looked up exactly (W^m = lo[m mod S] *
             // hi[m div S], m < N): W^(n2 t), W^(n2 T), W^(4 n2 T) and
@@ -743,10 +748,14 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
             // digits of g: eight table reads per thread instead of two per
             // point, at most six products deep.
             static_assert(K::P % 4 == 0 && K::P <= 32, "four-step columns hold 4 to 32 points per thread");
-            const float2 *lo = spec, *hi = spec + (1 << a.aux);
+            // the matched pass keeps its spectrum in spec and the table in tab2
+            // and multiplies by the conjugate factor (it ends with an inverse)
+            constexpr bool CONJ = INV || EPI == EPI_MATCHED_Y;
+            const float2 *tab = EPI == EPI_MATCHED_Y ? a.tab2 : spec;
+            const float2 *lo = tab, *hi = tab + (1 << a.aux);
             const int mask = (1 << a.aux) - 1;
             // the column's index, or for EPI_TWIDDLE_Y the problem's
-            const int n2 = EPI == EPI_TWIDDLE_Y ? (int)blockIdx.y : (int)(blk * K::C) + (valid ? c : 0);
+            const int n2 = EPI == EPI_TWIDDLE ? (int)(blk * K::C) + (valid ? c : 0) : (int)blockIdx.y;
             auto look = [&](int m) { return cmul(lo[m & mask], hi[m >> a.aux]); };
             float2 cf[4];
             cf[0] = look(n2 * t);
@@ -772,7 +781,7 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
                 static_for<0, 4>([&](auto jc) {
                     constexpr int i = 4 * g + decltype(jc)::value;
                     const float2 w = g == 0 ? cf[decltype(jc)::value] : cmul(cf[decltype(jc)::value], h);
-                    v[i] = INV ? cmulc(v[i], w) : cmul(v[i], w);
+                    v[i] = CONJ ? cmulc(v[i], w) : cmul(v[i], w);
                 });
             });
         }

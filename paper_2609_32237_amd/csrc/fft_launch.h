@@ -24,6 +24,10 @@ enum { LAYOUT_ROWS = 0, LAYOUT_COLS = 1, LAYOUT_RCMC = 2, LAYOUT_ROWS_HALF = 3 }
 //                azimuth filter), the inverse transform runs, and the result
 //                is written as columns; `spec` points to the range-Doppler
 //                tables below.
+//   EPI_MATCHED_Y  the middle pass of a matched filter along long columns in
+//                four-step form: forward, X[k] * conj(spec[y + (k << spec_shift)])
+//                * scale, inverse, then output j times conj(W^(y j)) from tab2
+//                (y = blockIdx.y);
 //   EPI_TWIDDLE_Y  middle pass of a three-pass transform: plain column strips,
 //                output point k of problem blockIdx.y times W^(blockIdx.y k)
 //                (the same two-level tables as EPI_TWIDDLE);
@@ -34,7 +38,15 @@ enum { LAYOUT_ROWS = 0, LAYOUT_COLS = 1, LAYOUT_RCMC = 2, LAYOUT_ROWS_HALF = 3 }
 //                m < N / S, with S = 2^aux.
 // Block -> strip maps of column kernels over the 8 XCDs (logical_block).
 enum { XCD_NONE = 0, XCD_CONTIG = 1, XCD_GROUPS = 2 };
-enum { EPI_NONE = 0, EPI_MATCHED = 1, EPI_SCALE = 2, EPI_RCMC = 3, EPI_TWIDDLE = 4, EPI_TWIDDLE_Y = 5 };
+enum {
+    EPI_NONE = 0,
+    EPI_MATCHED = 1,
+    EPI_SCALE = 2,
+    EPI_RCMC = 3,
+    EPI_TWIDDLE = 4,
+    EPI_TWIDDLE_Y = 5,
+    EPI_MATCHED_Y = 6
+};
 
 // Range-Doppler tables, one device block in this order (byte offsets from
 // rd_tables_layout; the interpolator rows are copied in from `interp_src`):
@@ -77,6 +89,11 @@ struct KArgs {
     // EPI_TWIDDLE with a row permutation: transform m of the batch is written
     // as row ((m mod 2^perm_b) << perm_a) | (m >> perm_b) (0, 0: row m)
     int perm_a, perm_b;
+    // EPI_MATCHED_Y: the spectrum value of point k is spec[blockIdx.y +
+    // (k << spec_shift)], and tab2 is the two-level table (log2 split aux) of
+    // the outer transform's factors
+    int spec_shift;
+    const float2 *tab2;
 };
 
 // Fills the addressing fields of `a` for workgroups of `c` transforms of `n`

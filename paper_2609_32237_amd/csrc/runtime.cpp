@@ -616,6 +616,69 @@ size_t sar_workspace_bytes(int64_t n_az, int64_t n_rg, int inter_storage) {
     return spectra + (size_t)n_az * (size_t)n_rg * el;
 }
 
+// An azimuth pass over 8192- or 16384-point columns holds one or two columns
+// per workgroup (8- or 16-byte pieces of each row).  With FP32 intermediates
+// it runs instead as three passes of short columns in the four-step form
+// (n_az = n1 * n2, n1 = 128, j = n2 j1 + j2, k = k1 + n1 k2), each reading
+// and writing wide pieces of the rows:
+//   B1  for each j2: 128-point FFTs down rows n2 j1 + j2, output k1 times
+//       W^(j2 k1), to rows j2 n1 + k1 of the workspace;
+//   B2  in place, for each k1: n2-point FFT down rows j2 n1 + k1 (giving
+//       X[k1 + n1 k2]), times conj(H_a[k1 + n1 k2]) / n_az, n2-point inverse
+//       FFT, output j2 times conj(W^(j2 k1));
+//   B3  for each j2: 128-point inverse FFTs down rows j2 n1 + k1, output j1 to
+//       row n2 j1 + j2 of the image.
+// The range pass then writes its result into `out`, which B1 reads.  A forced
+// column shape (MI355FFT_COL_VARIANT) keeps the single column pass.
+static bool long_azimuth(int64_t n_az, int inter_storage) {
+    const char *cv = std::getenv("MI355FFT_COL_VARIANT");
+    if (cv && cv[0]) return false;
+    return inter_storage == FFT_STORAGE_FP32 && (n_az == 8192 || n_az == 16384);
+}
+
+static int sar_long_azimuth(int64_t n_az, int64_t n_rg, const void *raw, void *out, void *mid, const float2 *h_rg,
+                     const float2 *h_az, const float2 *tw_rg, int vrow, int device, hipStream_t stream) {
+    using mi355fft::LAYOUT_COLS;
+    const int64_t n1 = 128, n2 = n_az / n1;
+    const float2 *tw1 = nullptr, *tw2 = nullptr, *ftab = nullptr;
+    const int log2s = (ilog2(n_az) + 1) / 2;
+    int rc = get_twiddles(device, n1, &tw1);
+    if (rc == FFT_OK) rc = get_twiddles(device, n2, &tw2);
+    if (rc == FFT_OK) rc = get_fourstep_table(device, n_az, log2s, &ftab);
+    if (rc != FFT_OK) return rc;
+    // range pass into `out`
+    const KArgs ar{n_az, 1, n_rg, n_rg, (float)(1.0 / (double)n_rg), 0};
+    hipError_t e = launch_fft(n_rg, vrow, mi355fft::LAYOUT_ROWS, FFT_STORAGE_FP32, FFT_STORAGE_FP32, 0,
+                              mi355fft::EPI_MATCHED, raw, out, tw_rg, h_rg, ar, stream);
+    if (e != hipSuccess) return map_hip(e);
+    KArgs b1{n_rg, n2 * n_rg, 1, 1, 1.0f, strip_map(n2 * n_rg * 8)};
+    b1.out_stride = n_rg;
+    b1.outer = (int)n2;
+    b1.outer_in_dist = n_rg;
+    b1.outer_out_dist = n1 * n_rg;
+    b1.aux = log2s;
+    e = launch_fft(n1, -1, LAYOUT_COLS, FFT_STORAGE_FP32, FFT_STORAGE_FP32, 0, mi355fft::EPI_TWIDDLE_Y, out, mid, tw1,
+                   ftab, b1, stream);
+    if (e != hipSuccess) return map_hip(e);
+    KArgs b2{n_rg, n1 * n_rg, 1, 1, (float)(1.0 / (double)n_az), strip_map(n1 * n_rg * 8)};
+    b2.outer = (int)n1;
+    b2.outer_in_dist = b2.outer_out_dist = n_rg;
+    b2.aux = log2s;
+    b2.spec_shift = ilog2(n1);
+    b2.tab2 = ftab;
+    e = launch_fft(n2, -1, LAYOUT_COLS, FFT_STORAGE_FP32, FFT_STORAGE_FP32, 0, mi355fft::EPI_MATCHED_Y, mid, mid, tw2,
+                   h_az, b2, stream);
+    if (e != hipSuccess) return map_hip(e);
+    KArgs b3{n_rg, n_rg, 1, 1, 1.0f, strip_map(n_rg * 8)};
+    b3.out_stride = n2 * n_rg;
+    b3.outer = (int)n2;
+    b3.outer_in_dist = n1 * n_rg;
+    b3.outer_out_dist = n_rg;
+    e = launch_fft(n1, -1, LAYOUT_COLS, FFT_STORAGE_FP32, FFT_STORAGE_FP32, 1, mi355fft::EPI_NONE, mid, out, tw1,
+                   nullptr, b3, stream);
+    return map_hip(e);
+}
+
 int sar_form_image_ex(int64_t n_az, int64_t n_rg, int inter_storage, const void *raw, const void *range_ref,
                       const void *az_ref, void *out, void *workspace, hipStream_t stream) {
     if (!raw || !range_ref || !az_ref || !out || !workspace) return FFT_EINVAL;
@@ -666,6 +729,10 @@ int sar_form_image_ex(int64_t n_az, int64_t n_rg, int inter_storage, const void 
         const KArgs a2{1, 1, n_az, n_az, 1.0f, 0};
         e = launch_fft(n_az, vref, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, az_ref, h_az, tw_az, nullptr, a2, stream);
         if (e != hipSuccess) return map_hip(e);
+    }
+
+    if (long_azimuth(n_az, inter_storage)) {
+        return sar_long_azimuth(n_az, n_rg, raw, out, mid, h_rg, h_az, tw_rg, vrow, device, stream);
     }
 
     // pass 1, rows (range): FFT, * conj(H_r) / n_rg, IFFT -> intermediate
