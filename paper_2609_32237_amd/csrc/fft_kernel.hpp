@@ -754,7 +754,8 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
             const float2 *tab = EPI == EPI_MATCHED_Y ? a.tab2 : spec;
             const float2 *lo = tab, *hi = tab + (1 << a.aux);
             const int mask = (1 << a.aux) - 1;
-            // the column's index, or for EPI_TWIDDLE_Y the problem's
+            // the column's index, or for the forms keyed by the grid's second
+            // axis (EPI_TWIDDLE_Y, EPI_MATCHED_Y) that axis's index
             const int n2 = EPI == EPI_TWIDDLE ? (int)(blk * K::C) + (valid ? c : 0) : (int)blockIdx.y;
             auto look = [&](int m) { return cmul(lo[m & mask], hi[m >> a.aux]); };
             float2 cf[4];
