@@ -93,6 +93,22 @@ def test_in_place(api, n, storage):
     assert rel_rows(y, oracle.fft(x)).max() < TOL[storage]
 
 
+@pytest.mark.parametrize("n", [8192, 16384])
+@pytest.mark.parametrize("storage", ["fp32", "fp16"])
+def test_long_columns_in_and_out_of_place(api, n, storage):
+    """Long interleaved columns run as two passes of short columns out of
+    place and as one pass in place; both against the oracle, ragged width."""
+    log(f"long columns n={n} {storage}")
+    cols, width = 70, 72
+    m = make_input(storage, (n, width), 700 + n)
+    ref = oracle.fft_layout(m, n, cols, width, 1, -1).reshape(n, width)
+    for inplace in (False, True):
+        y = run_plan(api, m, n, cols, width, 1, storage, -1, inplace=inplace)
+        err = rel_rows(widen(y).T[:cols], ref.T[:cols])
+        assert err.max() < TOL[storage], (inplace, err.max())
+        assert np.array_equal(y[:, cols:], m[:, cols:])
+
+
 @pytest.mark.parametrize("n", [1024, 4096, 16384])
 def test_padded_rows_and_strided_blocks(api, n):
     """dist > n leaves the gaps alone; stride 3 with dist 3n uses the column kernel on blocks."""

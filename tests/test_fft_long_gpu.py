@@ -42,7 +42,7 @@ def run(lib, x, n, batch, dist, storage, direction, out=None):
     return to_host(od)
 
 
-@pytest.mark.parametrize("log2n", [15, 16, 17, 18, 19, 20, 21, 22])
+@pytest.mark.parametrize("log2n", [15, 16, 17, 18, 19, 20, 21, 22, 23])
 @pytest.mark.parametrize("storage", [0, 1])
 def test_long_transforms_match_oracle(lib, log2n, storage):
     n = 1 << log2n
