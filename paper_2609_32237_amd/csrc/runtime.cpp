@@ -323,10 +323,10 @@ int64_t split_batch(int64_t n) {
 // 16-byte pieces of each row, while 64- and 128-point column kernels hold
 // 32-64 columns.  A forced column shape (MI355FFT_COL_VARIANT) keeps the
 // single pass.
-bool column_split(int64_t n, int64_t dist, int storage_layout_cols) {
+bool column_split(int64_t n, int64_t stride, int64_t dist) {
     const char *cv = std::getenv("MI355FFT_COL_VARIANT");
     if (cv && cv[0]) return false;
-    return storage_layout_cols && dist == 1 && (n == 8192 || n == 16384);
+    return stride > 1 && dist == 1 && (n == 8192 || n == 16384);
 }
 
 bool overlaps(const void *a, size_t na, const void *b, size_t nb) {
@@ -402,7 +402,7 @@ int fft_plan_create_ex(int64_t n, int64_t batch, int64_t stride, int64_t dist, i
     // na * nb, na = 2^floor(log2 n2 / 2).  Measured on MI355X (1 GiB,
     // 16 B/pt): 2^23 1.74 against 1.59 TB/s, 2^24 1.81 against 1.69,
     // 2^28 1.25 against 0.47; at 2^20-2^22 two passes stay ahead.
-    const bool colsplit = !half_x && !mfma && stride > 1 && column_split(n, dist, 1);
+    const bool colsplit = !half_x && !mfma && column_split(n, stride, dist);
     const bool split = four_step || may_split || colsplit;
     const bool three = four_step && n > kMaxTwoPass;
     // long columns: n1 = 128, n2 = 64 or 128
