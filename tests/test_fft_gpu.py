@@ -281,3 +281,47 @@ def test_sar_reference_buffers_in_either_order(api, order):
     ref = oracle.sar_chain(sc.raw, sc.range_ref, sc.az_ref)
     got = to_host(img).astype(np.complex128)
     assert np.linalg.norm(got - ref) / np.linalg.norm(ref) < 1e-5
+
+
+def test_one_plan_from_several_host_threads(api):
+    """One plan executed concurrently from four host threads, each on its own
+    stream and buffers (the plan is read-only after creation, the per-device
+    tables are shared), against the oracle, while each thread also creates,
+    uses and destroys a plan of its own."""
+    import threading
+
+    import torch
+
+    n, batch = 4096, 256
+    xs = [workloads.uniform_complex(batch, n, 600 + i) for i in range(4)]
+    refs = [oracle.fft(x) for x in xs]
+    p = api.Plan(n, batch, 1, n, 0, -1)
+    results, errors = [None] * 4, []
+
+    def work(i):
+        try:
+            s = torch.cuda.Stream()
+            with torch.cuda.stream(s):
+                xd = torch.from_numpy(xs[i]).to("cuda", non_blocking=False)
+                yd = torch.empty_like(xd)
+                for _ in range(5):
+                    p.execute(xd, yd, stream=s)
+                q = api.Plan(2048, 8, 1, 2048, 0, -1)
+                q.execute(xd[:8, :2048].contiguous(), torch.empty(8, 2048, dtype=torch.complex64, device="cuda"),
+                          stream=s)
+                s.synchronize()
+                q.close()
+                results[i] = yd.cpu().numpy()
+        except Exception as e:  # noqa: BLE001 - reported below
+            errors.append(repr(e))
+
+    log("plan from four host threads")
+    ts = [threading.Thread(target=work, args=(i,)) for i in range(4)]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
+    p.close()
+    assert not errors, errors
+    for i in range(4):
+        assert rel_rows(results[i].astype(np.complex128), refs[i]).max() < TOL["fp32"], i
