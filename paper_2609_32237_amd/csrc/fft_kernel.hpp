@@ -423,15 +423,26 @@ __device__ __forceinline__ void store_points(const float2 (&v)[K::P], void *__re
 //   exact rounding error (FMA), reduced by its nearest integer (exact), plus
 //   the cross terms; the reduced phase is then accurate to about 1e-7 cycles.
 //
-// The C range bins of the workgroup share their taps: for each Doppler bin k
-// the rows n0 + s0 - 3 .. n0 + s0 + C + 6 (s0 = floor(dn) of range bin n0,
+// The C range bins of the workgroup share their taps.  Where each thread has
+// at least two Doppler bins (P / C >= 2) and C >= 2, the gather runs by
+// column: thread tau takes Doppler bins k = tau + THREADS*m and, for each,
+// loads the window of C + 8 rows below into registers (one row per load
+// instruction of the wave: contiguous pieces) and interpolates all C range
+// bins from it, each point's eight taps starting 0 or 1 rows further down the
+// window than those of the point before; the results go to LDS in natural
+// order, half of the Doppler bins at a time (C * N / 2 complex values fit
+// where one component of the exchange does), and each thread reads back its
+// own points k = t + T*i.  Per point that is 16 bytes of LDS traffic for the
+// taps instead of 72 when they are staged, and four barriers in all.
+// Otherwise (one Doppler bin per thread)
+// for each Doppler bin k the rows n0 + s0 - 3 .. n0 + s0 + C + 4 (s0 = floor(dn) of range bin n0,
 // never larger than that of the others since dn grows with R0) hold every tap
-// of all C points, as long as dn varies by at most one bin across the strip
-// (the host guarantees it).  Doppler bins are processed in chunks of T (the
-// thread's own k for each i): the workgroup stages the chunk's W >= C + 10
-// rows into LDS (each thread loads W / C of them for its k, one row per load
-// instruction of the wave: contiguous pieces), then each thread reads its
-// eight taps from there.  G chunks share a barrier and two buffers of them
+// of all C points, as long as dn changes by less than one bin across the
+// strip (the host guarantees it), so that floor(dn) - s0 is 0 or 1.  Doppler
+// bins are processed in chunks of T (the thread's own k for each i): the
+// workgroup stages the chunk's W >= C + 8 rows into LDS (each thread loads
+// W / C of them for its k, one row per load instruction of the wave:
+// contiguous pieces), then each thread reads its eight taps from there.  G chunks share a barrier and two buffers of them
 // alternate, so one barrier per G chunks separates writing a buffer from
 // reading it, and the next G chunks' loads are in flight while the current
 // ones are computed.
@@ -442,18 +453,34 @@ __device__ __forceinline__ void store_points(const float2 (&v)[K::P], void *__re
 // hardware returns zero for them, which is the value the swath has there.
 template <class K>
 struct RcmcStage {
-    // at least C + 10 rows, rounded up to whole loads per thread (a load
+    // at least C + 8 rows, rounded up to whole loads per thread (a load
     // under a lane condition costs the compiler far more than the row)
-    static constexpr int LOADS = (K::C + 10 + K::C - 1) / K::C;  // rows each thread loads
+    static constexpr int LOADS = (K::C + 8 + K::C - 1) / K::C;  // rows each thread loads
     static constexpr int W = LOADS * K::C;                        // staged rows per Doppler bin
     static constexpr int FLOATS = 2 * W * K::T;                   // one chunk, complex
-    // staging pays when the strip shares taps (C >= 4) and two buffers fit
-    static constexpr bool ON = K::C >= 4 && 2 * FLOATS <= K::LDS_FLOATS;
+    // the column gather: two or more Doppler bins per thread and a strip of
+    // two or more range bins to share the window
+    static constexpr bool COLUMN = K::C >= 2 && K::P / K::C >= 2;
+    // otherwise staging pays when the strip shares taps (C >= 4) and two
+    // buffers fit
+    static constexpr bool ON = !COLUMN && K::C >= 4 && 2 * FLOATS <= K::LDS_FLOATS;
     // chunks staged per barrier: as many as two buffers of them fit (1, 2 or 4)
     static constexpr int G = (K::P % 4 == 0 && 8 * FLOATS <= K::LDS_FLOATS)   ? 4
                              : (K::P % 2 == 0 && 4 * FLOATS <= K::LDS_FLOATS) ? 2
                                                                              : 1;
 };
+
+// The azimuth filter applied to an interpolated value: acc times
+// exp(+j 2 pi cycles), cycles = R0 * rate from their hi/lo parts.
+__device__ __forceinline__ float2 rcmc_rotate(float2 acc, float2 r0, float4 rw) {
+    const float p = r0.x * rw.y;
+    const float e = fmaf(r0.x, rw.y, -p);
+    const float frac = (p - rintf(p)) + (e + fmaf(r0.x, rw.z, r0.y * rw.y));
+    // |frac| <= 1/2 + 2^-20: the hardware sine and cosine take the angle in
+    // revolutions (measured on this range: absolute error below 1.3e-7)
+    const float sn = __builtin_amdgcn_sinf(frac), cs = __builtin_amdgcn_cosf(frac);
+    return make_float2(acc.x * cs - acc.y * sn, acc.x * sn + acc.y * cs);
+}
 
 // Point i of thread (t, c): interpolation of the taps z(j) = Z[n + s - 3 + j]
 // with the blended table row, times the azimuth filter.
@@ -475,13 +502,38 @@ __device__ __forceinline__ float2 rcmc_point(float dn, float2 r0, float4 rw, con
         acc.x = fmaf(w1, z1.x, acc.x);
         acc.y = fmaf(w1, z1.y, acc.y);
     });
-    const float p = r0.x * rw.y;
-    const float e = fmaf(r0.x, rw.y, -p);
-    const float frac = (p - rintf(p)) + (e + fmaf(r0.x, rw.z, r0.y * rw.y));
-    // |frac| <= 1/2 + 2^-20: the hardware sine and cosine take the angle in
-    // revolutions (measured on this range: absolute error below 1.3e-7)
-    const float sn = __builtin_amdgcn_sinf(frac), cs = __builtin_amdgcn_cosf(frac);
-    return make_float2(acc.x * cs - acc.y * sn, acc.x * sn + acc.y * cs);
+    return rcmc_rotate(acc, r0, rw);
+}
+
+// The same point from a window of rows held in registers: its taps are
+// win[CI + d + j], d = 0 or 1.  Rather than selecting eight taps, the
+// weights are shifted: nine weights w'_i = (d ? w_(i-1) : w_i), with
+// w_(-1) = w_8 = 0, over win[CI .. CI + 8].
+template <int CI, int W>
+__device__ __forceinline__ float2 rcmc_point_win(float dn, bool d, float2 r0, float4 rw, const float4 *itab,
+                                                 const float2 (&win)[W]) {
+    static_assert(CI + 9 <= W, "the window holds every tap");
+    constexpr int RS = 5;
+    const float fd = floorf(dn);
+    const float qf = (dn - fd) * (float)kRcmcSub;
+    const int q = (int)qf;
+    const float al = qf - (float)q;
+    float w[8];
+    static_for<0, 4>([&](auto mc) {
+        constexpr int m = decltype(mc)::value;
+        const float4 g = itab[q * RS + m];
+        w[2 * m] = fmaf(al, g.y, g.x);
+        w[2 * m + 1] = fmaf(al, g.w, g.z);
+    });
+    float2 acc = make_float2(0.0f, 0.0f);
+    static_for<0, 9>([&](auto ic) {
+        constexpr int i = decltype(ic)::value;
+        const float lo = i < 8 ? w[i < 8 ? i : 0] : 0.0f, hi = i > 0 ? w[i > 0 ? i - 1 : 0] : 0.0f;
+        const float wi = d ? hi : lo;
+        acc.x = fmaf(wi, win[CI + i].x, acc.x);
+        acc.y = fmaf(wi, win[CI + i].y, acc.y);
+    });
+    return rcmc_rotate(acc, r0, rw);
 }
 
 template <class K, int ST>
@@ -513,7 +565,41 @@ __device__ __forceinline__ void rcmc_load(float2 (&v)[K::P], const void *__restr
     // integer part of a shift, kept at most n_rg so that no row offset wraps
     auto shift = [&](float dn) { return (int)fminf(floorf(dn), (float)n_rg); };
 
-    if constexpr (!S::ON) {
+    if constexpr (S::COLUMN) {
+        constexpr int C = K::C, M = P / C, TH = K::THREADS, WR = C + 8, HN = K::N / 2;
+        float2 *X = reinterpret_cast<float2 *>(lds);
+        static_assert(C * K::N <= K::LDS_FLOATS, "half of the points fit the exchange buffer");
+        // R0 of the strip's range bins (past the last one: the last one's)
+        float2 r0s[C];
+        static_for<0, C>([&](auto cc) { r0s[cc] = cols[min(n0 + (int)decltype(cc)::value, n_rg - 1)]; });
+        const int tau = threadIdx.x;
+        auto gather = [&](auto mc) {
+            constexpr int m = decltype(mc)::value;
+            const int k = tau + TH * m;
+            const float4 rw = rows[k];
+            const int s0 = shift(r0s[0].x * rw.x);
+            const unsigned off = (unsigned)(n0 + s0 - 3) * rb + (unsigned)(k * EL);
+            float2 win[WR];
+            static_for<0, WR>([&](auto uc) {
+                win[uc] = Store<ST>::load(r, off + (unsigned)decltype(uc)::value * rb, 0u);
+            });
+            float2 *dst = X + (k - (m >= M / 2 ? HN : 0));
+            static_for<0, C>([&](auto cc) {
+                constexpr int ci = decltype(cc)::value;
+                const float dn = r0s[ci].x * rw.x;
+                dst[ci * HN] = rcmc_point_win<ci>(dn, shift(dn) != s0, r0s[ci], rw, itab, win);
+            });
+        };
+        __syncthreads();  // itab
+        static_for<0, M / 2>(gather);
+        __syncthreads();
+        static_for<0, P / 2>([&](auto ic) { v[ic] = X[c * HN + t + T * decltype(ic)::value]; });
+        __syncthreads();
+        static_for<M / 2, M>(gather);
+        __syncthreads();
+        static_for<P / 2, P>([&](auto ic) { v[ic] = X[c * HN + t + T * decltype(ic)::value - HN]; });
+        __syncthreads();  // the transform's first exchange writes over X
+    } else if constexpr (!S::ON) {
         // each point reads its own eight rows
         float4 rw[P];
         static_for<0, P>([&](auto ic) { rw[ic] = rows[t + T * decltype(ic)::value]; });
@@ -571,7 +657,7 @@ __device__ __forceinline__ void rcmc_load(float2 (&v)[K::P], const void *__restr
                 constexpr int i = b * G + gc;
                 const float dn = r0.x * rwc[gc].x;
                 // this point's rows sit c + (s - s0) rows into the window
-                const int d = min(shift(dn) - shift(r00 * rwc[gc].x), 2);
+                const int d = min(shift(dn) - shift(r00 * rwc[gc].x), 1);
                 const float2 *zs = stage + ((i / G) & 1) * HALF + (i % G) * (S::FLOATS / 2) + (c + d) * T + t;
                 v[i] = rcmc_point<K>(dn, r0, rwc[gc], itab, [&](int j) { return zs[j * T]; });
             });

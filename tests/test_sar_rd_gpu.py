@@ -66,6 +66,12 @@ SMALL = dict(
                         targets=((512, 128, 1.0), (1024, 640, 1.0), (1536, 384, 0.8), (1536, 700, 1.0))),
     wide_1024x2048=dict(n_rg=2048, pulse_samples=600,
                         targets=((256, 300, 1.0), (512, 1400, 1.0), (768, 900, 0.6))),
+    # long azimuth at the paper's PRF (1500-pulse apertures): the
+    # migration-correction kernels with 4 and 2 range bins per strip
+    long_8192x1024=dict(n_az=8192, prf=500.0,
+                        targets=((1024, 128, 1.0), (4096, 640, 1.0), (6000, 384, 0.8))),
+    long_16384x1024=dict(n_az=16384, prf=500.0,
+                         targets=((2048, 300, 1.0), (8192, 700, 1.0), (12000, 500, 0.8))),
 )
 
 
@@ -126,7 +132,7 @@ def test_repeat_calls_and_caller_workspace(api):
 
 
 @pytest.mark.parametrize("var", ["MI355FFT_COL_VARIANT", "MI355FFT_RCMC_VARIANT"])
-@pytest.mark.parametrize("shape", ["square_1024", "tall_2048x1024"])
+@pytest.mark.parametrize("shape", ["square_1024", "tall_2048x1024", "long_8192x1024", "long_16384x1024"])
 def test_every_kernel_variant(api, var, shape):
     """The azimuth FFT (column kernels) and the migration-correction pass
     (its own kernel list) with every shape, forced through the variant
