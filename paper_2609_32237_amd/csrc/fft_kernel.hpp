@@ -591,11 +591,11 @@ __device__ __forceinline__ void rcmc_load(float2 (&v)[K::P], const void *__restr
             });
         };
         __syncthreads();  // itab
-        static_for<0, M / 2>(gather);
+        static_for<0, M / 2>(gather);  // Doppler bins [0, N/2)
         __syncthreads();
         static_for<0, P / 2>([&](auto ic) { v[ic] = X[c * HN + t + T * decltype(ic)::value]; });
-        __syncthreads();
-        static_for<M / 2, M>(gather);
+        __syncthreads();  // the first half is read; the second overwrites it
+        static_for<M / 2, M>(gather);  // Doppler bins [N/2, N)
         __syncthreads();
         static_for<P / 2, P>([&](auto ic) { v[ic] = X[c * HN + t + T * decltype(ic)::value - HN]; });
         __syncthreads();  // the transform's first exchange writes over X
@@ -805,8 +805,9 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
     if constexpr (!K::PERSIST) {
         // strips per 128-byte line, from the narrower of the two sides' pieces;
         // the migration pass keeps groups of at least 8 strips on an XCD, since
-        // neighbouring strips also read overlapping windows of rows (FETCH_SIZE
-        // 1.3x its input instead of 2.1x with groups of 2)
+        // neighbouring strips also read overlapping windows of rows (with the
+        // taps staged in LDS, FETCH_SIZE was 1.3x its input against 2.1x with
+        // groups of 2)
         constexpr int PIECE = K::C * (Store<IN_ST>::BYTES < Store<OUT_ST>::BYTES ? Store<IN_ST>::BYTES
                                                                                 : Store<OUT_ST>::BYTES);
         constexpr int LINE_GROUP = PIECE >= 128 ? 1 : 128 / PIECE;
