@@ -159,3 +159,32 @@ def test_every_kernel_variant(api, var, shape):
             log(f"rd {shape} {var}={v} inter={inter}: rel {e:.3e}")
             assert e < TOL[inter], (v, inter, e)
         v += 1
+
+
+def test_paper_scene_every_migration_kernel(api, paper_scene):
+    """Every migration-correction kernel of the 4096-point list (8 range bins
+    and 32 points per thread, 4 range bins and 16 points per thread), forced
+    through MI355FFT_RCMC_VARIANT, on the 4096 x 4096 scene: the same bounds
+    and exact peak positions."""
+    import os
+
+    from paper_2609_32237_amd import _lib
+
+    sc, ref = paper_scene
+    v = 0
+    while True:
+        os.environ["MI355FFT_RCMC_VARIANT"] = str(v)
+        try:
+            try:
+                got = [form(api, sc, inter) for inter in (0, 1)]
+            except _lib.FFTError as e:
+                assert e.code == _lib.FFT_EINVAL and v >= 2
+                break
+        finally:
+            os.environ.pop("MI355FFT_RCMC_VARIANT", None)
+        for inter in (0, 1):
+            e = rel(got[inter].astype(np.complex128), ref)
+            log(f"rd paper scene MI355FFT_RCMC_VARIANT={v} inter={inter}: rel {e:.3e}")
+            assert e < TOL[inter], (v, inter, e)
+            check_peaks(got[inter], ref, sc)
+        v += 1
