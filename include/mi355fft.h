@@ -142,8 +142,8 @@ enum { FFT_FLAG_FP16_EXCHANGE = 1, FFT_FLAG_MATRIX_UNITS = 2 };
  *               kernel measured 66 dB).  Requires FFT_STORAGE_FP16 (else
  *               FFT_EINVAL), stride == 1, n = 4096 or 16384 and scale_log2 = 0
  *               (else FFT_EUNSUPPORTED); exclusive with the FP16 exchange.
- *               Slower than the default kernels on MI355X (1.1x the time at
- *               n = 4096, 1.6x at 16384, from HBM): an experiment, opt-in.
+ *               Slower than the default kernels on MI355X (1.2x the time at
+ *               n = 4096, 1.7x at 16384, from HBM): an experiment, opt-in.
  *               Unknown flags give FFT_EINVAL.
  * Other arguments, tables and errors as fft_plan_create.
  */
