@@ -76,8 +76,11 @@ struct Configs<1024> {
                        KCfg<1024, 16, 1, false, XCHG_FULL, 1, false, Radices<16, 16, 4>>>;
     using Cols = KList<KCfg<1024, 16, 8, true, XCHG_SPLIT, 1, false, Radices<16, 16, 4>>,
                        KCfg<1024, 16, 8, true, XCHG_FULL, 0, false, Radices<16, 16, 4>>>;
-    using Rcmc = KList<KCfg<1024, 16, 16, false, XCHG_SPLIT, 1, false, Radices<16, 16, 4>>,
-                       KCfg<1024, 16, 8, false, XCHG_SPLIT, 1, false, Radices<16, 16, 4>>>;
+    // 8 range bins per strip: 229 against 256 us for 16 (which held one
+    // Doppler bin per thread, too few for the column gather) on a 1024 x 16384
+    // range-Doppler chain
+    using Rcmc = KList<KCfg<1024, 16, 8, false, XCHG_SPLIT, 1, false, Radices<16, 16, 4>>,
+                       KCfg<1024, 16, 4, false, XCHG_SPLIT, 1, false, Radices<16, 16, 4>>>;
     using RowsHalf = KList<KCfg<1024, 16, 4, false, XCHG_HALF, 1, false, Radices<16, 16, 4>>>;
     static constexpr int kRowDefault[2] = {1, 0}, kColDefault[2] = {0, 0};
     static constexpr int kRowMatched = 1, kColMatched = 0;

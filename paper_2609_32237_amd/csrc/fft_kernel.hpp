@@ -423,52 +423,32 @@ __device__ __forceinline__ void store_points(const float2 (&v)[K::P], void *__re
 //   exact rounding error (FMA), reduced by its nearest integer (exact), plus
 //   the cross terms; the reduced phase is then accurate to about 1e-7 cycles.
 //
-// The C range bins of the workgroup share their taps.  Where each thread has
-// at least two Doppler bins (P / C >= 2) and C >= 2, the gather runs by
-// column: thread tau takes Doppler bins k = tau + THREADS*m and, for each,
-// loads the window of C + 8 rows below into registers (one row per load
+// The C range bins of the workgroup share their taps: for Doppler bin k the
+// rows n0 + s0 - 3 .. n0 + s0 + C + 4 (s0 = floor(dn) of range bin n0, never
+// larger than that of the others since dn grows with R0) hold every tap of
+// all C points, as long as dn changes by less than one bin across the strip
+// (the host guarantees it), so that floor(dn) - s0 is 0 or 1.  The gather
+// runs by column: thread tau takes Doppler bins k = tau + THREADS*m and, for
+// each, loads that window of C + 8 rows into registers (one row per load
 // instruction of the wave: contiguous pieces) and interpolates all C range
 // bins from it, each point's eight taps starting 0 or 1 rows further down the
 // window than those of the point before; the results go to LDS in natural
 // order, half of the Doppler bins at a time (C * N / 2 complex values fit
 // where one component of the exchange does), and each thread reads back its
-// own points k = t + T*i.  Per point that is 16 bytes of LDS traffic for the
-// taps instead of 72 when they are staged, and four barriers in all.
-// Otherwise (one Doppler bin per thread)
-// for each Doppler bin k the rows n0 + s0 - 3 .. n0 + s0 + C + 4 (s0 = floor(dn) of range bin n0,
-// never larger than that of the others since dn grows with R0) hold every tap
-// of all C points, as long as dn changes by less than one bin across the
-// strip (the host guarantees it), so that floor(dn) - s0 is 0 or 1.  Doppler
-// bins are processed in chunks of T (the thread's own k for each i): the
-// workgroup stages the chunk's W >= C + 8 rows into LDS (each thread loads
-// W / C of them for its k, one row per load instruction of the wave:
-// contiguous pieces), then each thread reads its eight taps from there.  G chunks share a barrier and two buffers of them
-// alternate, so one barrier per G chunks separates writing a buffer from
-// reading it, and the next G chunks' loads are in flight while the current
-// ones are computed.
+// own points k = t + T*i: 16 bytes of LDS traffic per point and four
+// barriers in all.  A kernel with one range bin per workgroup (C = 1) has
+// nothing to share, and each point loads its own eight rows.
 // The image is addressed through one buffer resource spanning its n_rg rows
 // (the host guarantees it fits 31 bits), each row with its own 32-bit offset:
 // rows outside [0, n_rg) fall outside the resource (a negative row wraps to an
 // offset above 2^31, a row past the end lies past the span), and the
 // hardware returns zero for them, which is the value the swath has there.
+// The column gather needs two or more Doppler bins per thread (the two
+// halves) and a strip of two or more range bins to share the window.
 template <class K>
-struct RcmcStage {
-    // at least C + 8 rows, rounded up to whole loads per thread (a load
-    // under a lane condition costs the compiler far more than the row)
-    static constexpr int LOADS = (K::C + 8 + K::C - 1) / K::C;  // rows each thread loads
-    static constexpr int W = LOADS * K::C;                        // staged rows per Doppler bin
-    static constexpr int FLOATS = 2 * W * K::T;                   // one chunk, complex
-    // the column gather: two or more Doppler bins per thread and a strip of
-    // two or more range bins to share the window
-    static constexpr bool COLUMN = K::C >= 2 && K::P / K::C >= 2;
-    // otherwise staging pays when the strip shares taps (C >= 4) and two
-    // buffers fit
-    static constexpr bool ON = !COLUMN && K::C >= 4 && 2 * FLOATS <= K::LDS_FLOATS;
-    // chunks staged per barrier: as many as two buffers of them fit (1, 2 or 4)
-    static constexpr int G = (K::P % 4 == 0 && 8 * FLOATS <= K::LDS_FLOATS)   ? 4
-                             : (K::P % 2 == 0 && 4 * FLOATS <= K::LDS_FLOATS) ? 2
-                                                                             : 1;
-};
+constexpr bool rcmc_column() {
+    return K::C >= 2 && K::P / K::C >= 2;
+}
 
 // The azimuth filter applied to an interpolated value: acc times
 // exp(+j 2 pi cycles), cycles = R0 * rate from their hi/lo parts.
@@ -542,7 +522,7 @@ __device__ __forceinline__ void rcmc_load(float2 (&v)[K::P], const void *__restr
                                           float *lds) {
     static_assert(!K::COLS && !K::PERSIST, "the migration correction reads rows of the transposed image");
     static_assert(kRcmcTaps == 8, "four float4 per table row");
-    using S = RcmcStage<K>;
+    static_assert(rcmc_column<K>() || K::C == 1, "a strip of range bins takes the column gather");
     constexpr int EL = Store<ST>::BYTES, P = K::P, T = K::T;
     // table row q holds {g_j, dg_j, g_j+1, dg_j+1} for j = 0, 2, 4, 6 in four
     // float4 slots of a five-slot stride: consecutive rows start 20 banks
@@ -558,14 +538,13 @@ __device__ __forceinline__ void rcmc_load(float2 (&v)[K::P], const void *__restr
     for (int e = threadIdx.x; e < (kRcmcSub + 1) * 4; e += K::THREADS) itab[(e >> 2) * RS + (e & 3)] = interp[e];
     const int n0 = (int)(blk * K::C);
     const int n = n0 + (valid ? c : 0);  // lanes past the last column redo the block's first
-    const float r00 = cols[n0].x;
     const float2 r0 = cols[n];
     const unsigned rb = (unsigned)(a.in_dist * EL);
     const rsrc_t r = make_rsrc(in, (unsigned)((long long)n_rg * a.in_dist * EL));
     // integer part of a shift, kept at most n_rg so that no row offset wraps
     auto shift = [&](float dn) { return (int)fminf(floorf(dn), (float)n_rg); };
 
-    if constexpr (S::COLUMN) {
+    if constexpr (rcmc_column<K>()) {
         constexpr int C = K::C, M = P / C, TH = K::THREADS, WR = C + 8, HN = K::N / 2;
         float2 *X = reinterpret_cast<float2 *>(lds);
         static_assert(C * K::N <= K::LDS_FLOATS, "half of the points fit the exchange buffer");
@@ -599,8 +578,8 @@ __device__ __forceinline__ void rcmc_load(float2 (&v)[K::P], const void *__restr
         __syncthreads();
         static_for<P / 2, P>([&](auto ic) { v[ic] = X[c * HN + t + T * decltype(ic)::value - HN]; });
         __syncthreads();  // the transform's first exchange writes over X
-    } else if constexpr (!S::ON) {
-        // each point reads its own eight rows
+    } else {
+        // one range bin per workgroup: each point reads its own eight rows
         float4 rw[P];
         static_for<0, P>([&](auto ic) { rw[ic] = rows[t + T * decltype(ic)::value]; });
         __syncthreads();  // itab
@@ -610,65 +589,6 @@ __device__ __forceinline__ void rcmc_load(float2 (&v)[K::P], const void *__restr
             const unsigned off = (unsigned)(n + shift(dn) - 3) * rb + (unsigned)((t + T * i) * EL);
             v[i] = rcmc_point<K>(dn, r0, rw[i], itab,
                                  [&](int j) { return Store<ST>::load(r, off + (unsigned)j * rb, 0u); });
-        });
-    } else {
-        float2 *stage = reinterpret_cast<float2 *>(lds);
-        constexpr int G = S::G, HALF = G * (S::FLOATS / 2);  // float2 per buffer
-        auto fetch = [&](int i, float4 rwi, float2 (&z)[S::LOADS]) {
-            const unsigned off = (unsigned)(n0 + shift(r00 * rwi.x) - 3) * rb + (unsigned)((t + T * i) * EL);
-            static_for<0, S::LOADS>([&](auto uc) {
-                constexpr int u = decltype(uc)::value;
-                z[u] = Store<ST>::load(r, off + (unsigned)(c + u * K::C) * rb, 0u);
-            });
-        };
-        // chunk i lives in buffer (i / G) & 1, slot i % G
-        auto put = [&](int i, const float2 (&z)[S::LOADS]) {
-            float2 *dst = stage + ((i / G) & 1) * HALF + (i % G) * (S::FLOATS / 2) + t;
-            static_for<0, S::LOADS>([&](auto uc) {
-                constexpr int u = decltype(uc)::value;
-                dst[(c + u * K::C) * T] = z[u];
-            });
-        };
-        // row-table entries rotate through three register sets of G: chunks
-        // being computed, chunks whose rows are in flight, chunks being read
-        float4 rwc[G], rwn[G];
-        static_for<0, G>([&](auto gc) {
-            rwc[gc] = rows[t + T * decltype(gc)::value];
-            rwn[gc] = P / G > 1 ? rows[t + T * (G + decltype(gc)::value)] : rwc[gc];
-        });
-        static_for<0, G>([&](auto gc) {
-            float2 z[S::LOADS];
-            fetch(gc, rwc[gc], z);
-            put(gc, z);
-        });
-        __syncthreads();  // itab and the first G chunks
-        static_for<0, P / G>([&](auto bc) {
-            constexpr int b = decltype(bc)::value;
-            float4 rwf[G];
-            static_for<0, G>([&](auto gc) {
-                rwf[gc] = rwn[gc];
-                if constexpr (b + 2 < P / G) rwf[gc] = rows[t + T * ((b + 2) * G + decltype(gc)::value)];
-            });
-            float2 zn[G][S::LOADS];
-            if constexpr (b + 1 < P / G) {
-                static_for<0, G>([&](auto gc) { fetch((b + 1) * G + gc, rwn[gc], zn[gc]); });
-            }
-            static_for<0, G>([&](auto gc) {
-                constexpr int i = b * G + gc;
-                const float dn = r0.x * rwc[gc].x;
-                // this point's rows sit c + (s - s0) rows into the window
-                const int d = min(shift(dn) - shift(r00 * rwc[gc].x), 1);
-                const float2 *zs = stage + ((i / G) & 1) * HALF + (i % G) * (S::FLOATS / 2) + (c + d) * T + t;
-                v[i] = rcmc_point<K>(dn, r0, rwc[gc], itab, [&](int j) { return zs[j * T]; });
-            });
-            if constexpr (b + 1 < P / G) {
-                static_for<0, G>([&](auto gc) { put((b + 1) * G + gc, zn[gc]); });
-            }
-            __syncthreads();  // the next G chunks staged; these G chunks' buffer free
-            static_for<0, G>([&](auto gc) {
-                rwc[gc] = rwn[gc];
-                rwn[gc] = rwf[gc];
-            });
         });
     }
 }
