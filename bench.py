@@ -11,13 +11,23 @@ time of the K timed steps.  The JSON line also carries:
                 stream), against the 8 TB/s HBM peak; ``traffic`` comes from the
                 committed rocprofv3 FETCH_SIZE/WRITE_SIZE measurement when it
                 was taken on the current kernel sources, else null;
-  cpu_baseline  the fp64 oracle timed on this host on a bounded sample of the
-                same workload;
+                ``measured_copy_GBs`` is the best 1 GiB read+write copy of the
+                membench kernels timed the same way, the ceiling the access
+                pattern of a one-read-one-write kernel can reach on this GPU;
+  cpu_baseline  the fp64 oracle timed on this host, one thread and all the
+                process's cores, on a bounded sample of the same workload and
+                on one whole SAR image;
   breakdown     the other workloads (N = 1024 latency case, 8192, 16384, FP16
-                storage, a 2^20-point transform in the two-pass four-step form, the 4096 x 4096 two-pass SAR image and the 4096 x
-                4096 full range-Doppler image of the paper's L-band scene, with
-                FP32 and FP16 intermediates), each a median of cache-flushed
-                samples.
+                storage, a 2^20-point transform in the two-pass four-step
+                form, the 4096 x 4096 two-pass SAR image and the 4096 x 4096
+                full range-Doppler image of the paper's L-band scene, with FP32
+                and FP16 intermediates), each the median of cache-flushed
+                samples interleaved across the workloads after a clock warm-up;
+  traffic_by_kernel  HBM bytes per launch of every FFT kernel from the
+                committed FETCH_SIZE/WRITE_SIZE run, when it was taken on the
+                current kernel sources.
+Modes: --ceilings (memory-system ceilings), --experiment matrix-units,
+--summarize / --lds-summary / --make-traffic (rocprofv3 output to profiles/).
 """
 from __future__ import annotations
 
@@ -49,7 +59,7 @@ def kernel_source_digest() -> str:
     csrc = os.path.join(ROOT, "paper_2609_32237_amd", "csrc")
     h = hashlib.sha256()
     for name in sorted(os.listdir(csrc)):
-        if name.endswith((".hip", ".hpp", ".h")):
+        if name.endswith((".hip", ".hpp", ".h")) and not name.startswith("membench"):
             h.update(name.encode())
             h.update(open(os.path.join(csrc, name), "rb").read())
     return h.hexdigest()[:16]
@@ -90,7 +100,31 @@ def time_samples(torch, fn, flush, samples, warmup=2):
     return float(np.median(ms)), float(np.percentile(ms, 25)), float(np.percentile(ms, 75))
 
 
-def fft_breakdown(torch, api, flush, name, samples):
+def time_interleaved(torch, cases, flush, samples, warm_s=2.0):
+    """Section III's protocol: every sample is one call after a cache flush, and
+    the samples of the workloads are interleaved (round r times every workload
+    once), after a clock warm-up that runs them all, so that clock and thermal
+    drift spread over all of them alike.  Returns {name: array of ms}."""
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < warm_s:
+        for c in cases:
+            flush()
+            c["fn"]()
+        torch.cuda.synchronize()
+    ev = {c["name"]: [] for c in cases}
+    for _ in range(samples):
+        for c in cases:
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            flush()
+            a.record()
+            c["fn"]()
+            b.record()
+            ev[c["name"]].append((a, b))
+        torch.cuda.synchronize()
+    return {k: np.array([a.elapsed_time(b) for a, b in v]) for k, v in ev.items()}
+
+
+def fft_case(torch, api, name):
     import workloads
 
     w = workloads.FFT_WORKLOADS[name]
@@ -98,46 +132,60 @@ def fft_breakdown(torch, api, flush, name, samples):
     x = torch.from_numpy(workloads.fft_workload(name)).cuda()
     out = torch.empty_like(x)
     plan = api.Plan(n, batch, 1, n, 0 if storage == "fp32" else 1, -1)
-    med, q1, q3 = time_samples(torch, lambda: plan.execute(x, out), flush, samples)
-    plan.close()
-    bytes_ = 2 * n * batch * (8 if storage == "fp32" else 4)
-    del x, out
-    torch.cuda.empty_cache()
-    gbs = bytes_ / (med * 1e-3) / 1e9
-    return {"n": n, "batch": batch, "storage": storage, "ms_median": round(med, 5), "ms_iqr": [round(q1, 5), round(q3, 5)],
-            "GB/s": round(gbs, 1), "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
-            "GFLOPS": round(gflops(n, batch, med * 1e-3), 1)}
+    return {"name": name, "fn": lambda: plan.execute(x, out), "keep": (x, out, plan),
+            "bytes": 2 * n * batch * (8 if storage == "fp32" else 4), "flops": 5.0 * n * np.log2(n) * batch,
+            "meta": {"n": n, "batch": batch, "storage": storage}}
 
 
-def matrix_unit_experiment(torch, api, flush, samples):
-    """FP16 storage, 1 GiB batches: the vector kernels (FP32 exchange), the FP16
-    exchange and the radix-16 butterflies on the matrix cores (Section VIII)."""
-    res = {"experiment": "matrix-units", "storage": "fp16", "results": []}
-    g = torch.Generator(device="cuda").manual_seed(12)
-    t0 = time.perf_counter()
-    while time.perf_counter() - t0 < 2.0:  # a fresh process: bring the clocks up first
-        for _ in range(20):
-            flush()
-        torch.cuda.synchronize()
-    for n in (4096, 16384):
-        batch = (1 << 30) // (n * 4)
-        x = (torch.rand(batch, n, 2, device="cuda", generator=g) * 2 - 1).half()
+def cross_lane_experiment(torch, api, flush, samples):
+    """The exchange between stages made across the lanes of one wave (no LDS,
+    no barrier) against the LDS exchanges, on 1 GiB batches of 1024-point rows
+    in FP32 and FP16 storage (Section VI's exchange, re-designed for a 64-lane
+    wave).  Each kernel shape is forced by its index in the 1024-point row
+    list; flushed samples are interleaved across the shapes after a clock
+    warm-up, and a back-to-back rate (20 launches) is taken as for ``value``."""
+    shapes = {0: "LDS, split exchange, 4 transforms per workgroup",
+              1: "LDS, full exchange, 4 transforms per workgroup",
+              4: "LDS, full exchange, 1 transform per workgroup (one wave, no barrier)",
+              5: "cross-lane, 4 transforms per workgroup",
+              6: "cross-lane, 1 transform per workgroup"}
+    res = {"experiment": "cross-lane", "n": 1024, "results": []}
+    g = torch.Generator(device="cuda").manual_seed(13)
+    for storage in (0, 1):
+        el = 8 if storage == 0 else 4
+        batch = (1 << 30) // (1024 * el)
+        x = torch.rand(batch, 1024, 2, device="cuda", generator=g) * 2 - 1
+        x = torch.view_as_complex(x) if storage == 0 else x.half()
         out = torch.empty_like(x)
-        for name, flags in (("vector", 0), ("fp16_exchange", api._lib.FFT_FLAG_FP16_EXCHANGE),
-                            ("matrix_units", api._lib.FFT_FLAG_MATRIX_UNITS)):
-            plan = api.Plan(n, batch, 1, n, 1, -1, flags=flags)
-            med, q1, q3 = time_samples(torch, lambda: plan.execute(x, out), flush, samples)
-            plan.close()
-            gbs = 8 * n * batch / (med * 1e-3) / 1e9
-            res["results"].append({"n": n, "batch": batch, "kernels": name, "ms_median": round(med, 5),
-                                   "ms_iqr": [round(q1, 5), round(q3, 5)], "GB/s": round(gbs, 1),
-                                   "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)})
+        cases = []
+        for v, what in shapes.items():
+            os.environ["MI355FFT_ROW_VARIANT"] = str(v)
+            try:
+                plan = api.Plan(1024, batch, 1, 1024, storage, -1)
+            finally:
+                os.environ.pop("MI355FFT_ROW_VARIANT", None)
+            cases.append({"name": str(v), "fn": (lambda p=plan: p.execute(x, out)), "plan": plan, "what": what})
+        ms = time_interleaved(torch, cases, flush, samples)
+        for c in cases:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(20):
+                c["fn"]()
+            e1.record()
+            torch.cuda.synchronize()
+            b2b = e0.elapsed_time(e1) / 20
+            med = float(np.median(ms[c["name"]]))
+            res["results"].append({"storage": "fp32" if storage == 0 else "fp16", "batch": batch,
+                                   "row_variant": int(c["name"]), "kernel": c["what"],
+                                   "flushed_ms": round(med, 5), "flushed_GB/s": round(2 * (1 << 30) / (med * 1e-3) / 1e9, 1),
+                                   "back_to_back_GB/s": round(2 * (1 << 30) / (b2b * 1e-3) / 1e9, 1)})
+            c["plan"].close()
         del x, out
         torch.cuda.empty_cache()
     return res
 
 
-def long_breakdown(torch, api, flush, n, batch, samples):
+def long_case(torch, api, n, batch):
     """A transform longer than the chip holds: the two-pass four-step form.
     GB/s counts the method's own 16 bytes per point (one read, one write);
     the two passes move twice that."""
@@ -145,15 +193,12 @@ def long_breakdown(torch, api, flush, n, batch, samples):
     x = torch.view_as_complex(torch.rand(batch, n, 2, device="cuda", generator=g) * 2 - 1)
     out = torch.empty_like(x)
     plan = api.Plan(n, batch, 1, n, 0, -1)
-    med, q1, q3 = time_samples(torch, lambda: plan.execute(x, out), flush, samples)
-    plan.close()
-    gbs = 16 * n * batch / (med * 1e-3) / 1e9
-    return {"n": n, "batch": batch, "storage": "fp32", "passes": 2, "ms_median": round(med, 5),
-            "ms_iqr": [round(q1, 5), round(q3, 5)], "GB/s": round(gbs, 1), "moved_GB/s": round(2 * gbs, 1),
-            "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4), "GFLOPS": round(gflops(n, batch, med * 1e-3), 1)}
+    return {"name": f"fft_n{n}_b{batch}_fp32", "fn": lambda: plan.execute(x, out), "keep": (x, out, plan),
+            "bytes": 16 * n * batch, "flops": 5.0 * n * np.log2(n) * batch,
+            "meta": {"n": n, "batch": batch, "storage": "fp32", "passes": 2, "moved_bytes": 32 * n * batch}}
 
 
-def sar_breakdown(torch, api, flush, inter, samples):
+def sar_case(torch, api, inter):
     import workloads
 
     sc = workloads.sar_scene()
@@ -162,17 +207,15 @@ def sar_breakdown(torch, api, flush, inter, samples):
     ha = torch.from_numpy(sc.az_ref).cuda()
     out = torch.empty_like(raw)
     ws = torch.empty(api._lib.sar_workspace_bytes(4096, 4096, inter), dtype=torch.uint8, device="cuda")
-    fn = lambda: api.sar_form_image(raw, hr, ha, inter, out=out, workspace=ws)  # noqa: E731
-    med, q1, q3 = time_samples(torch, fn, flush, samples)
     bpp = 32 if inter == 0 else 24  # raw read + intermediate write + read + image write
-    bytes_ = bpp * 4096 * 4096
-    gbs = bytes_ / (med * 1e-3) / 1e9
-    return {"image": "4096x4096", "intermediate": "fp32" if inter == 0 else "fp16", "ms_median": round(med, 5),
-            "ms_iqr": [round(q1, 5), round(q3, 5)], "algorithmic_bytes_per_point": bpp, "GB/s": round(gbs, 1),
-            "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)}
+    return {"name": f"sar_4096x4096_{'fp32' if inter == 0 else 'fp16'}_inter",
+            "fn": lambda: api.sar_form_image(raw, hr, ha, inter, out=out, workspace=ws),
+            "keep": (raw, hr, ha, out, ws), "bytes": bpp * 4096 * 4096,
+            "meta": {"image": "4096x4096", "intermediate": "fp32" if inter == 0 else "fp16",
+                     "algorithmic_bytes_per_point": bpp}}
 
 
-def rd_breakdown(torch, api, flush, inter, samples):
+def rd_case(torch, api, inter):
     """The paper's full range-Doppler chain on its 4096 x 4096 L-band scene."""
     import workloads
 
@@ -181,66 +224,277 @@ def rd_breakdown(torch, api, flush, inter, samples):
     hr = torch.from_numpy(sc.range_ref).cuda()
     out = torch.empty_like(raw)
     ws = torch.empty(api._lib.sar_rd_workspace_bytes(4096, 4096, inter), dtype=torch.uint8, device="cuda")
-    fn = lambda: api.sar_rd_form_image(raw, hr, sc.geometry, inter, out=out, workspace=ws)  # noqa: E731
-    med, q1, q3 = time_samples(torch, fn, flush, samples)
     # raw read, range-compressed write + read, range-Doppler write + read, image write
     bpp = 48 if inter == 0 else 32
-    gbs = bpp * 4096 * 4096 / (med * 1e-3) / 1e9
-    return {"image": "4096x4096", "scene": "L-band stripmap, 6 targets (Section X)",
-            "intermediate": "fp32" if inter == 0 else "fp16", "passes": 3, "ms_median": round(med, 5),
-            "ms_iqr": [round(q1, 5), round(q3, 5)], "algorithmic_bytes_per_point": bpp, "GB/s": round(gbs, 1),
-            "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)}
+    return {"name": f"rd_4096x4096_{'fp32' if inter == 0 else 'fp16'}_inter",
+            "fn": lambda: api.sar_rd_form_image(raw, hr, sc.geometry, inter, out=out, workspace=ws),
+            "keep": (raw, hr, out, ws), "bytes": bpp * 4096 * 4096,
+            "meta": {"image": "4096x4096", "scene": "L-band stripmap, 6 targets (Section X)",
+                     "intermediate": "fp32" if inter == 0 else "fp16", "passes": 3,
+                     "algorithmic_bytes_per_point": bpp}}
 
 
-def cpu_baseline(x_host, n, target_s=10.0):
-    """The fp64 oracle on a bounded sample of the workload, on this host's cores
-    (median of three timings of the same sample)."""
-    import oracle
+def breakdown(torch, api, flush, samples, copy_gbs):
+    cases = []
+    for name in ("fft_n1024_b64_fp32", "fft_n4096_b32768_fp32", "fft_n8192_b16384_fp32",
+                 "fft_n16384_b8192_fp32", "fft_n16384_b16384_fp16"):
+        log(f"breakdown: preparing {name}")
+        cases.append(fft_case(torch, api, name))
+    cases.append(long_case(torch, api, 1 << 20, 128))
+    for inter in (0, 1):
+        cases.append(sar_case(torch, api, inter))
+    for inter in (0, 1):
+        cases.append(rd_case(torch, api, inter))
+    log(f"breakdown: {len(cases)} workloads, {samples} interleaved flushed samples each")
+    ms = time_interleaved(torch, cases, flush, samples)
+    bd = {}
+    for c in cases:
+        m = ms[c["name"]]
+        med = float(np.median(m))
+        gbs = c["bytes"] / (med * 1e-3) / 1e9
+        r = dict(c["meta"])
+        r.update({"ms_median": round(med, 5),
+                  "ms_iqr": [round(float(np.percentile(m, 25)), 5), round(float(np.percentile(m, 75)), 5)],
+                  "GB/s": round(gbs, 1), "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+                  "frac_of_measured_copy": round(gbs / copy_gbs, 4)})
+        if "flops" in c:
+            r["GFLOPS"] = round(c["flops"] / (med * 1e-3) / 1e9, 1)
+        bd[c["name"]] = r
+    del cases
+    torch.cuda.empty_cache()
+    return bd
 
-    threads = oracle.default_threads()
-    probe = 256
-    t0 = time.perf_counter()
-    oracle.fft(x_host[:probe], nthreads=threads)
-    t_probe = time.perf_counter() - t0
-    count = int(min(x_host.shape[0], max(probe, probe * target_s / 3 / max(t_probe, 1e-6))))
-    xs = x_host[:count].astype(np.complex128)  # widening is not timed
+
+def host_info():
+    """This host's CPU model, the processor count the OS reports, the CPUs this
+    process may run on, and the thread count the all-core runs use: the
+    process's CPU share (OMP_NUM_THREADS when set, as on a one-GPU machine where it
+    is 16 whatever nproc says), never more than the CPUs it may run on."""
+    model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    affinity = len(os.sched_getaffinity(0))
+    share = os.environ.get("OMP_NUM_THREADS", "")
+    threads = min(affinity, int(share)) if share.isdigit() and int(share) > 0 else affinity
+    return {"cpu_model": model, "nproc": os.cpu_count(), "cpus_allowed": affinity,
+            "omp_num_threads": share or None, "threads_all_cores": threads}
+
+
+def _median_time(fn, reps=3):
     times = []
-    for _ in range(3):
+    for _ in range(reps):
         t0 = time.perf_counter()
-        oracle.fft_layout(xs, n, count, 1, n, -1, nthreads=threads)
+        fn()
         times.append(time.perf_counter() - t0)
-    dt = float(np.median(times))
-    return {"value": round(16.0 * n * count / dt / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {count} of {x_host.shape[0]} transforms (N={n}, fp64 radix-2), median of 3 "
-                      f"timings, {dt:.2f} s each"}
+    return float(np.median(times))
+
+
+def cpu_baseline(x_host, n, target_s=3.0):
+    """The fp64 oracle, as it stands, on this host: the benchmark's FFT workload
+    on a bounded sample of its transforms with one thread and with all the
+    process's cores (median of three timings each), and one whole 4096 x 4096
+    SAR image (the two-pass chain in fp64) likewise.  ``value`` is the
+    all-core FFT rate in the metric's unit (algorithmic bytes, 16 per point)."""
+    import oracle
+    import workloads
+
+    info = host_info()
+    threads = info["threads_all_cores"]
+    probe = 64
+    t_probe = _median_time(lambda: oracle.fft(x_host[:probe], nthreads=1), reps=1)
+    count1 = int(min(x_host.shape[0], max(probe, probe * target_s / max(t_probe, 1e-6))))
+    count_all = int(min(x_host.shape[0], count1 * threads))
+    xs = x_host[:count_all].astype(np.complex128)  # widening is not timed
+    dt1 = _median_time(lambda: oracle.fft_layout(xs[:count1], n, count1, 1, n, -1, nthreads=1))
+    dta = _median_time(lambda: oracle.fft_layout(xs, n, count_all, 1, n, -1, nthreads=threads))
+    del xs
+    sc = workloads.sar_scene()
+    raw = sc.raw.astype(np.complex128)
+    s1 = _median_time(lambda: oracle.sar_chain(raw, sc.range_ref, sc.az_ref, nthreads=1))
+    sa = _median_time(lambda: oracle.sar_chain(raw, sc.range_ref, sc.az_ref, nthreads=threads))
+    gbs = lambda count, dt: round(16.0 * n * count / dt / 1e9, 4)  # noqa: E731
+    return {"value": gbs(count_all, dta), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {count_all} of {x_host.shape[0]} transforms (N={n}, fp64 radix-2) on {threads} "
+                      f"threads, median of 3 timings, {dta:.2f} s each; one thread: first {count1} "
+                      f"transforms, {dt1:.2f} s each",
+            "single_thread": {"value": gbs(count1, dt1), "unit": "GB/s", "transforms": count1,
+                              "seconds": round(dt1, 4)},
+            "all_cores": {"value": gbs(count_all, dta), "unit": "GB/s", "transforms": count_all,
+                          "seconds": round(dta, 4), "threads": threads},
+            "sar_4096x4096_ms": {"single_thread": round(s1 * 1e3, 1), "all_cores": round(sa * 1e3, 1),
+                                 "threads": threads, "chain": "two-pass, fp64, median of 3"},
+            "host": info}
+
+
+MB_COPY, MB_READ, MB_WRITE, MB_BLOCK, MB_STRIP = range(5)
+
+
+def membench_lib():
+    """The memory-ceiling kernels (csrc/membench.hip), a library of their own."""
+    import ctypes
+
+    path = os.path.join(ROOT, "paper_2609_32237_amd", "libmi355membench.so")
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with __graft_entry__.build()")
+    lib = ctypes.CDLL(path)
+    c = ctypes
+    lib.mb_run.argtypes = [c.c_int, c.c_void_p, c.c_void_p, c.c_longlong, c.c_longlong, c.c_longlong, c.c_int,
+                           c.c_void_p]
+    lib.mb_run.restype = c.c_int
+    return lib
+
+
+def mb_time(torch, lib, kind, src, dst, nbytes, a, b, flags, launches=20, flush=None):
+    """Milliseconds per launch of one membench kernel: back to back (the mean of
+    `launches` launches between two events, as ``value`` is measured) or, with
+    `flush`, the median of single launches each after a cache flush."""
+    h = torch.cuda.current_stream().cuda_stream
+
+    def run():
+        rc = lib.mb_run(kind, src.data_ptr(), dst.data_ptr(), nbytes, a, b, flags, h)
+        if rc != 0:
+            raise RuntimeError(f"mb_run({kind}, bytes={nbytes}, a={a}, b={b}, flags={flags}) -> {rc}")
+
+    run()
+    torch.cuda.synchronize()
+    if flush is None:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(launches):
+            run()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / launches
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(launches)]
+    for e0, e1 in ev:
+        flush()
+        e0.record()
+        run()
+        e1.record()
+    torch.cuda.synchronize()
+    return float(np.median([e0.elapsed_time(e1) for e0, e1 in ev]))
 
 
 def copy_reference(torch):
-    """Read+write bandwidth of a plain streaming kernel on this GPU: an in-place
-    scale of a 1 GiB buffer (reads and writes every byte once), median of 10."""
-    buf = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
-    for _ in range(3):
-        buf.mul_(1.0)
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(10)]
-    for a, b in ev:
-        a.record()
-        buf.mul_(1.0)
-        b.record()
-    torch.cuda.synchronize()
-    ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
-    del buf
+    """The best read+write copy of 1 GiB each way on this GPU, timed like
+    ``value`` (20 launches back to back): one 16-byte access per lane, plain
+    and with non-temporal loads and stores.  Returns (GB/s, details)."""
+    lib = membench_lib()
+    nbytes = 1 << 30
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    res = {}
+    for name, flags in (("plain", 0), ("nontemporal", 3)):
+        ms = mb_time(torch, lib, MB_COPY, src, dst, nbytes, 1, 0, flags)
+        res[name] = round(2.0 * nbytes / (ms * 1e-3) / 1e9, 1)
+    del src, dst
     torch.cuda.empty_cache()
-    return 2.0 * (1 << 30) / (ms * 1e-3) / 1e9
+    return max(res.values()), {"kernel": "membench copy, 16 B per lane, 1 GiB each way, 20 back to back",
+                               "GB/s": res}
+
+
+def ceilings(torch, flush):
+    """Memory-system ceilings on this GPU (Section IV's bandwidth against working
+    set, scaled to MI355X): copy, read and write over working sets of 1 MiB to
+    8 GiB, each pass's chunks moved to another workgroup of the same XCD so
+    that small sets are served by the L2 or the Infinity Cache; then the FFT
+    kernels' own access patterns on 1 GiB each way (rows in 32 KiB blocks) and
+    on 4096-row matrices (column strips of C = 4, 8, 16)."""
+    lib = membench_lib()
+    out = {"sweep": [], "block": [], "strip": []}
+    big = 8 << 30
+    src = torch.ones(big // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    sums = torch.empty(1024, dtype=torch.float32, device="cuda")
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < 2.0:  # bring the clocks up first
+        mb_time(torch, lib, MB_COPY, src, dst, 1 << 30, 1, 0, 0, launches=5)
+    mib = 1
+    while mib <= 8192:
+        nbytes = mib << 20
+        # Up to 32 MiB (4 MiB of L2 per XCD) the passes run inside one launch,
+        # each workgroup's chunk moving to another workgroup of its XCD, so the
+        # data stays in that XCD's L2.  Larger sets take one pass per launch,
+        # launched back to back: the whole set is touched between two touches
+        # of any line, which leaves it in the Infinity Cache while it fits there
+        # (both buffers of a copy count) and in HBM beyond.
+        reps = max(1, (4 << 30) // nbytes) if mib <= 32 else 1
+        launches = 5 if mib <= 32 else max(5, (4 << 30) // nbytes)
+        row = {"MiB": mib, "passes_per_launch": reps, "launches": launches}
+        for name, kind, flags, moved, d in (("copy", MB_COPY, 0, 2, dst), ("copy_nt", MB_COPY, 3, 2, dst),
+                                            ("read", MB_READ, 0, 1, sums), ("write", MB_WRITE, 0, 1, dst)):
+            ms = mb_time(torch, lib, kind, src, d, nbytes, reps, 0, flags, launches=launches)
+            row[name] = round(moved * nbytes * reps / (ms * 1e-3) / 1e9, 1)
+        out["sweep"].append(row)
+        log(f"ceilings {mib} MiB: {row}")
+        mib *= 2
+    nbytes = 1 << 30
+    for lds_kib in (0, 34):
+        for flags, hint in ((0, "plain"), (3, "nontemporal")):
+            b2b = mb_time(torch, lib, MB_BLOCK, src, dst, nbytes, 16, lds_kib, flags, launches=20)
+            cold = mb_time(torch, lib, MB_BLOCK, src, dst, nbytes, 16, lds_kib, flags, launches=11, flush=flush)
+            out["block"].append({"pattern": "32 KiB block per 256-lane workgroup, 16 x 8 B per lane",
+                                 "lds_kib": lds_kib, "hint": hint,
+                                 "back_to_back_GB/s": round(2 * nbytes / (b2b * 1e-3) / 1e9, 1),
+                                 "flushed_GB/s": round(2 * nbytes / (cold * 1e-3) / 1e9, 1)})
+            log(f"ceilings block {out['block'][-1]}")
+    for width in (4096, 32768):
+        nbytes = 4096 * width * 8
+        for c in (4, 8, 16):
+            for mode, what in ((0, "strided reads and writes"), (1, "strided reads, contiguous writes"),
+                               (2, "contiguous reads, strided writes")):
+                cold = mb_time(torch, lib, MB_STRIP, src, dst, nbytes, width, c, mode, launches=11, flush=flush)
+                b2b = mb_time(torch, lib, MB_STRIP, src, dst, nbytes, width, c, mode, launches=20)
+                out["strip"].append({"rows": 4096, "width": width, "MiB_each_way": nbytes >> 20, "C": c,
+                                     "piece_bytes": 8 * c, "mode": what,
+                                     "flushed_GB/s": round(2 * nbytes / (cold * 1e-3) / 1e9, 1),
+                                     "back_to_back_GB/s": round(2 * nbytes / (b2b * 1e-3) / 1e9, 1)})
+                log(f"ceilings strip {out['strip'][-1]}")
+    del src, dst, sums
+    torch.cuda.empty_cache()
+    return out
+
+
+EPI_NAMES = {0: "plain", 1: "matched", 2: "scaled, transposed out", 3: "migration (RCMC)", 4: "four-step twiddled",
+             5: "twiddled (grid y)", 6: "matched (grid y)"}
+XCHG_NAMES = {0: "full", 1: "split", 2: "half", 3: "lane"}
+
+
+def kernel_label(name: str) -> str:
+    """Short label of an FFT kernel instantiation from its demangled name:
+    fft_kernel<KCfg<N, P, C, COLS, XCHG, TWMODE, PERSIST, Radices<...>, NTROW>,
+    IN_ST, OUT_ST, INV, EPI>; other kernels keep their name up to the first '('."""
+    import re
+
+    m = re.search(r"fft_kernel<mi355fft::KCfg<(\d+), (\d+), (\d+), (true|false), (\d+), (\d+), (true|false), "
+                  r"mi355fft::Radices<([\d, ]+)>, (true|false)>, (\d), (\d), (true|false), (\d)>", name)
+    if not m:
+        return name.split("(")[0].replace("void ", "")[:80]
+    n, p, c, cols, xchg, _tw, pers, rad, _nt, ist, ost, inv, epi = m.groups()
+    st = {"0": "fp32", "1": "fp16"}
+    return (f"N={n} {'cols' if cols == 'true' else 'rows'} C={c} P={p} {XCHG_NAMES.get(int(xchg), xchg)} "
+            f"[{rad.replace(' ', '')}]{' persistent' if pers == 'true' else ''} "
+            f"{EPI_NAMES.get(int(epi), epi)} {st[ist]}->{st[ost]}{' inv' if inv == 'true' else ''}")
+
+
+HEADLINE_KERNEL = "N=4096 rows C=1 P=16 full [16,16,16] plain fp32->fp32"
+TRAFFIC_FILE = os.path.join(PROFILES, "traffic_fft_kernels_bench_breakdown.json")
 
 
 def load_traffic(digest: str):
-    path = os.path.join(PROFILES, f"traffic_{WORKLOAD}.json")
-    if not os.path.exists(path):
+    """{kernel label: record} of the committed FETCH_SIZE/WRITE_SIZE
+    measurement when it was taken on the current kernel sources, else None."""
+    if not os.path.exists(TRAFFIC_FILE):
         return None
-    rec = json.load(open(path))
+    rec = json.load(open(TRAFFIC_FILE))
     if rec.get("kernel_source_digest") != digest:
         return None
-    return rec.get("bytes_per_launch")
+    return rec.get("kernels")
 
 
 def summarize(prof_dir: str, command: str) -> str:
@@ -274,43 +528,101 @@ def summarize(prof_dir: str, command: str) -> str:
     return "\n".join(lines) + "\n"
 
 
-def _pmc_means(prof_dir: str, counter: str):
-    """{(kernel name, grid): mean counter value per dispatch} from a --pmc run."""
+def _pmc_rows(prof_dir: str):
+    """Raw per-dispatch counter rows of a --pmc run: (dispatch id, kernel name,
+    grid size, counter, value)."""
     import csv
     import glob
-    from collections import defaultdict
 
-    vals = defaultdict(list)
+    rows = []
     for path in glob.glob(os.path.join(prof_dir, "**", "*counter_collection.csv"), recursive=True):
         for r in csv.DictReader(open(path)):
-            if r["Counter_Name"] == counter:
-                vals[(r["Kernel_Name"], int(r["Grid_Size"]))].append(float(r["Counter_Value"]))
-    return {k: float(np.mean(v)) for k, v in vals.items()}
+            rows.append((int(r.get("Dispatch_Id", 0) or 0), r["Kernel_Name"], int(r["Grid_Size"]),
+                         r["Counter_Name"], float(r["Counter_Value"])))
+    return rows
+
+
+def _per_dispatch(rows, counter):
+    """{(kernel name, grid): [value per dispatch]}: values of one counter summed
+    per dispatch (a counter collected per XCD or per instance may come as
+    several rows of one dispatch), then listed per kernel."""
+    from collections import defaultdict
+
+    per = defaultdict(float)
+    key_of = {}
+    for d, name, grid, cname, v in rows:
+        if cname == counter:
+            per[d] += v
+            key_of[d] = (name, grid)
+    out = defaultdict(list)
+    for d, v in per.items():
+        out[key_of[d]].append(v)
+    return out
 
 
 def make_traffic(fetch_dir: str, write_dir: str, commands: list) -> dict:
-    """HBM-side bytes per launch of the benchmarked FFT kernel from two --pmc runs
-    (FETCH_SIZE, WRITE_SIZE; KiB per dispatch), each scaled by what the same
-    counter reads for the copy-reference kernel, which reads and writes exactly
-    1 GiB per dispatch."""
-    rec = {"workload": WORKLOAD, "kernel_source_digest": kernel_source_digest(), "commands": commands}
-    n, batch = 4096, 32768
+    """HBM-side bytes per launch of every FFT kernel of a --pmc run over the
+    benchmark (FETCH_SIZE, WRITE_SIZE; KiB per dispatch), each counter scaled
+    by what it reads for the membench copy kernel of the same run, which reads
+    and writes exactly 1 GiB per dispatch."""
+    import statistics
+
+    rec = {"kernel_source_digest": kernel_source_digest(), "commands": commands, "kernels": {}}
+    vals = {}
     for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
-        means = _pmc_means(d, counter)
-        fft = [v for (name, grid), v in means.items() if "fft_kernel<mi355fft::KCfg<4096," in name
-               and grid == batch * 256 and "(mi355fft::EPI" not in name]
-        calib = [v for (name, grid), v in means.items() if "MulFunctor" in name and grid >= (1 << 26)]
-        if not fft or not calib:
-            raise RuntimeError(f"{counter}: benchmark or reference kernel missing in {d}")
-        factor = ((1 << 30) / 1024.0) / calib[0]
+        per = _per_dispatch(_pmc_rows(d), counter)
+        calib = [v for (name, grid), vs in per.items() for v in vs
+                 if "copy_kernel" in name and grid == (1 << 30) // 16]
+        if not calib:
+            raise RuntimeError(f"{counter}: reference copy kernel missing in {d}")
+        factor = ((1 << 30) / 1024.0) / statistics.median(calib)
         key = "fetch" if counter == "FETCH_SIZE" else "write"
-        rec[f"{key}_kib_per_dispatch_raw"] = fft[0]
-        rec[f"{key}_reference_kib_per_dispatch_raw"] = calib[0]
         rec[f"{key}_scale"] = factor
-        rec[f"{key}_bytes_per_launch"] = fft[0] * 1024.0 * factor
-    rec["algorithmic_bytes_per_launch"] = 16 * n * batch
-    rec["bytes_per_launch"] = rec["fetch_bytes_per_launch"] + rec["write_bytes_per_launch"]
+        rec[f"{key}_reference_kib_per_dispatch_raw"] = statistics.median(calib)
+        for (name, grid), vs in per.items():
+            if "fft_kernel" not in name:
+                continue
+            label = kernel_label(name) + f" grid={grid}"
+            vals.setdefault(label, {})[key] = statistics.mean(vs) * 1024.0 * factor
+    for label, v in sorted(vals.items()):
+        if "fetch" in v and "write" in v:
+            rec["kernels"][label] = {"fetch_bytes": round(v["fetch"]), "write_bytes": round(v["write"]),
+                                     "bytes_per_launch": round(v["fetch"] + v["write"])}
+    head = [k for k in rec["kernels"] if k.startswith(HEADLINE_KERNEL) and k.endswith(f"grid={32768 * 256}")]
+    if head:
+        rec["kernels"][HEADLINE_KERNEL] = rec["kernels"][head[0]]
     return rec
+
+
+def lds_summary(prof_dir: str, command: str) -> str:
+    """Per-kernel VALU and LDS counters per point from a --pmc run, each counter
+    summed over the rows of one dispatch first (the per-dispatch aggregation
+    the earlier table lacked), then averaged over the kernel's dispatches."""
+    import statistics
+
+    rows = _pmc_rows(prof_dir)
+    counters = sorted({r[3] for r in rows})
+    per = {c: _per_dispatch(rows, c) for c in counters}
+    lines = [f"command: {command}", f"source: {prof_dir}", "counters: " + " ".join(counters),
+             "per point: instructions x 64 / points of the dispatch (points = grid x points per lane)", ""]
+    keys = sorted({k for c in counters for k in per[c]}, key=lambda k: kernel_label(k[0]))
+    for name, grid in keys:
+        if "fft_kernel" not in name:
+            continue
+        label = kernel_label(name)
+        import re
+
+        m = re.search(r"KCfg<\d+, (\d+),", name)
+        pts = grid * int(m.group(1)) if m else grid
+        vals = {c: statistics.mean(per[c][(name, grid)]) for c in counters if (name, grid) in per[c]}
+        parts = []
+        for c in counters:
+            if c not in vals:
+                continue
+            v = vals[c]
+            parts.append(f"{c}={v:.4g}" + (f" ({v * 64 / pts:.2f}/pt)" if c.startswith("SQ_INSTS") else ""))
+        lines.append(f"{label} grid={grid}: " + ", ".join(parts))
+    return "\n".join(lines) + "\n"
 
 
 def main():
@@ -320,6 +632,9 @@ def main():
     if len(sys.argv) > 1 and sys.argv[1] == "--make-traffic":
         print(json.dumps(make_traffic(sys.argv[2], sys.argv[3], sys.argv[4:]), indent=1))
         return
+    if len(sys.argv) > 1 and sys.argv[1] == "--lds-summary":
+        print(lds_summary(sys.argv[2], " ".join(sys.argv[3:])), end="")
+        return
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
@@ -327,7 +642,10 @@ def main():
     ap.add_argument("--samples", type=int, default=11, help="cache-flushed samples per breakdown workload")
     ap.add_argument("--no-breakdown", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--experiment", choices=["matrix-units"], default=None,
+    ap.add_argument("--ceilings", action="store_true",
+                    help="instead of the benchmark: the memory-system ceilings (copy/read/write against working "
+                         "set, the FFT kernels' block and strip patterns), one JSON line")
+    ap.add_argument("--experiment", choices=["matrix-units", "cross-lane"], default=None,
                     help="instead of the benchmark: FP16-storage N = 4096 / 16384 with the vector kernels, the "
                          "FP16 exchange and the matrix-core butterflies (one JSON line)")
     args = ap.parse_args()
@@ -342,6 +660,12 @@ def main():
     from paper_2609_32237_amd import torch_api as api
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.ceilings:
+        print(json.dumps(ceilings(torch, Flusher(torch))), flush=True)
+        return
+    if args.experiment == "cross-lane":
+        print(json.dumps(cross_lane_experiment(torch, api, Flusher(torch), args.samples)), flush=True)
+        return
     if args.experiment == "matrix-units":
         print(json.dumps(matrix_unit_experiment(torch, api, Flusher(torch), args.samples)), flush=True)
         return
@@ -376,12 +700,15 @@ def main():
     plan.close()
     del x, out
     torch.cuda.empty_cache()
-    copy_gbs = copy_reference(torch)
+    copy_gbs, copy_info = copy_reference(torch)
+    traffic = load_traffic(digest)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": load_traffic(digest),
+                "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": traffic.get(HEADLINE_KERNEL, {}).get("bytes_per_launch") if traffic else None,
                 "kernel": "fft_kernel rows N=4096 fp32 forward", "algorithmic_bytes_per_launch": step_bytes,
                 "avg_launch_ms": round(kernel_ms, 5), "kernel_source_digest": digest,
-                "measured_copy_GBs": round(copy_gbs, 1), "frac_of_measured_copy": round(achieved / copy_gbs, 4)}
+                "measured_copy_GBs": round(copy_gbs, 1), "frac_of_measured_copy": round(achieved / copy_gbs, 4),
+                "measured_copy": copy_info}
     result = {
         "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(wall * 1e3 / args.steps, 5), "higher_is_better": True,
@@ -398,23 +725,9 @@ def main():
     del x_host
 
     if not args.no_breakdown:
-        flush = Flusher(torch)
-        bd = {}
-        for name in ("fft_n1024_b64_fp32", "fft_n4096_b32768_fp32", "fft_n8192_b16384_fp32",
-                     "fft_n16384_b8192_fp32", "fft_n16384_b16384_fp16"):
-            log(f"breakdown {name}")
-            bd[name] = fft_breakdown(torch, api, flush, name, args.samples)
-        log("breakdown fft_n1048576_b128_fp32 (four-step)")
-        bd["fft_n1048576_b128_fp32"] = long_breakdown(torch, api, flush, 1 << 20, 128, args.samples)
-        for inter in (0, 1):
-            log(f"breakdown sar inter={inter}")
-            bd[f"sar_4096x4096_{'fp32' if inter == 0 else 'fp16'}_inter"] = sar_breakdown(
-                torch, api, flush, inter, args.samples)
-        for inter in (0, 1):
-            log(f"breakdown range-Doppler inter={inter}")
-            bd[f"rd_4096x4096_{'fp32' if inter == 0 else 'fp16'}_inter"] = rd_breakdown(
-                torch, api, flush, inter, args.samples)
-        result["breakdown"] = bd
+        result["breakdown"] = breakdown(torch, api, Flusher(torch), args.samples, copy_gbs)
+        if traffic:
+            result["traffic_by_kernel"] = {k: v for k, v in traffic.items()}
     print(json.dumps(result), flush=True)
 
 

@@ -24,8 +24,11 @@
  *     pointer on the current HIP device; the caller owns it.
  *   - Every call is stream-ordered on the given hipStream_t (0 = the null
  *     stream) and never synchronises.  Argument errors are returned before
- *     any HIP call is made.  A failed launch returns FFT_EHIP.  Faults inside
- *     a kernel surface at the caller's next synchronisation.
+ *     any HIP call is made.  A failed launch returns FFT_EHIP; the status is
+ *     that of the library's own launch, read from the launch call itself, so
+ *     an earlier error the caller left pending is neither reported nor
+ *     cleared.  Faults inside a kernel surface at the caller's next
+ *     synchronisation.
  *   - Transforms are unnormalised in both directions: forward computes
  *     X[k] = sum_n x[n] exp(-2 pi i n k / N), inverse uses exp(+2 pi i n k / N).
  *     Output is in natural order.
@@ -128,6 +131,12 @@ enum { FFT_FLAG_FP16_EXCHANGE = 1, FFT_FLAG_MATRIX_UNITS = 2 };
  *               the caller keeps the block exponent: scale_log2 = log2(n)
  *               bounds every output of a forward transform by the largest
  *               input magnitude, whatever the data.  0 is fft_plan_create.
+ *               The split forms (four-step, long columns, small batches)
+ *               apply 2^-min(s, log2 n1) in their first pass, and with three
+ *               passes 2^-min(rest, log2 na) in the second, the rest in the
+ *               last, so that no intermediate stored in `out` grows past the
+ *               bound of the final outputs; each factor is exact, so the
+ *               results are those of one final scale.
  *   flags       0, or FFT_FLAG_FP16_EXCHANGE: the exchange between stages is
  *               stored as binary16 pairs instead of FP32 (Section VII's
  *               FP16-exchange variant: half the on-chip traffic of the FP32
@@ -156,12 +165,19 @@ int fft_plan_create_ex(int64_t n, int64_t batch, int64_t stride, int64_t dist, i
  * Every transform is read from `in` once and written to `out` once (Section
  * VI: the whole transform stays on chip between its stages).
  *   in, out  device buffers laid out as the plan says; in == out (in place) is
- *            allowed for n <= 16384 (FFT_EINVAL for longer transforms),
- *            partial overlap is not.  Aligned to one complex element
- *            (8 bytes FP32, 4 bytes FP16), else FFT_EALIGN.
+ *            allowed for n <= 16384 (FFT_EINVAL for longer transforms).
+ *            Otherwise the two extents, (batch-1)*dist + (n-1)*stride + 1
+ *            elements from each pointer, must be disjoint, else FFT_EINVAL.
+ *            Aligned to one complex element (8 bytes FP32, 4 bytes FP16),
+ *            else FFT_EALIGN.
  *   stream   HIP stream the kernel is launched on.
+ * The current HIP device must be the one the plan was created on (its tables
+ * live there), else FFT_EINVAL.
  * Safe to call concurrently on different streams with the same plan.
- * Returns FFT_OK, FFT_EINVAL (NULL plan or buffer), FFT_EALIGN or FFT_EHIP.
+ * Returns FFT_OK, FFT_EINVAL (NULL plan or buffer, overlapping extents, other
+ * device), FFT_EALIGN or FFT_EHIP (the status of the launch itself: an
+ * earlier, unrelated HIP error of the calling thread is neither returned nor
+ * cleared).
  */
 int fft_execute(const fft_plan *plan, const void *in, void *out, hipStream_t stream);
 

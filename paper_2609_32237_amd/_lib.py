@@ -29,8 +29,8 @@ FFT_FLAG_FP16_EXCHANGE = 1
 FFT_FLAG_MATRIX_UNITS = 2
 
 EXPORTS = ("fft_plan_create", "fft_plan_create_ex", "fft_execute", "fft_plan_destroy", "sar_workspace_bytes",
-           "sar_form_image_ex", "sar_form_image", "sar_rd_workspace_bytes", "sar_rd_form_image",
-           "fft_strerror")
+           "sar_form_image_ex", "sar_form_image", "sar_rd_workspace_bytes",
+           "sar_rd_form_image", "fft_strerror")
 
 
 class SarGeometry(ctypes.Structure):

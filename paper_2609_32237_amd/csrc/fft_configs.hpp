@@ -73,7 +73,11 @@ struct Configs<1024> {
                        KCfg<1024, 16, 4, false, XCHG_FULL, 1, false, Radices<16, 16, 4>>,
                        KCfg<1024, 16, 4, false, XCHG_FULL, 1, true, Radices<16, 16, 4>>,
                        KCfg<1024, 16, 4, false, XCHG_FULL, 0, false, Radices<16, 16, 4>>,
-                       KCfg<1024, 16, 1, false, XCHG_FULL, 1, false, Radices<16, 16, 4>>>;
+                       KCfg<1024, 16, 1, false, XCHG_FULL, 1, false, Radices<16, 16, 4>>,
+                       // every exchange across the lanes of one wave, no LDS:
+                       // four transforms (waves) or one per workgroup
+                       KCfg<1024, 16, 4, false, XCHG_LANE, 1, false, Radices<16, 16, 4>>,
+                       KCfg<1024, 16, 1, false, XCHG_LANE, 1, false, Radices<16, 16, 4>>>;
     using Cols = KList<KCfg<1024, 16, 8, true, XCHG_SPLIT, 1, false, Radices<16, 16, 4>>,
                        KCfg<1024, 16, 8, true, XCHG_FULL, 0, false, Radices<16, 16, 4>>>;
     // 8 range bins per strip: 229 against 256 us for 16 (which held one
@@ -285,7 +289,15 @@ hipError_t dispatch_cfg_full(int in_st, int out_st, int inv, int epi, const void
 template <class K>
 hipError_t dispatch_cfg(int in_st, int out_st, int inv, int epi, const void *in, void *out, const float2 *tw,
                         const float2 *spec, const KArgs &a, hipStream_t s) {
-    if constexpr (K::XCHG == XCHG_HALF) {
+    if constexpr (K::XCHG == XCHG_LANE) {
+        // the cross-lane exchange: plain row transforms, either storage
+        if (epi != EPI_NONE || in_st != out_st) return hipErrorInvalidValue;
+        if (in_st == 0)
+            return inv ? launch_one<K, 0, 0, true, EPI_NONE>(in, out, tw, spec, a, s)
+                       : launch_one<K, 0, 0, false, EPI_NONE>(in, out, tw, spec, a, s);
+        return inv ? launch_one<K, 1, 1, true, EPI_NONE>(in, out, tw, spec, a, s)
+                   : launch_one<K, 1, 1, false, EPI_NONE>(in, out, tw, spec, a, s);
+    } else if constexpr (K::XCHG == XCHG_HALF) {
         // the binary16 exchange: FP16 storage, plain transforms only
         if (epi != EPI_NONE || in_st != 1 || out_st != 1) return hipErrorInvalidValue;
         return inv ? launch_one<K, 1, 1, true, EPI_NONE>(in, out, tw, spec, a, s)

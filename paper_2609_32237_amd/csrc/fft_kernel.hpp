@@ -24,6 +24,9 @@
 //          HALF: the complex value rounded to a binary16 pair (N*4 bytes, one
 //          round; Section VII's FP16 exchange, about 6 dB less accurate, for
 //          FP16 storage only).
+//          LANE: no LDS: each wave holds one 1024-point transform and every
+//          exchange is a register/lane transpose made with cross-lane
+//          instructions (fft_lane.hpp).
 //   TWMODE 0: every inter-stage twiddle read from the table;
 //          1: one table read per base-4 digit of the radix, the rest formed
 //          by complex products (fewer loads, a few more FP32 operations).
@@ -46,7 +49,7 @@
 
 namespace mi355fft {
 
-enum { XCHG_FULL = 0, XCHG_SPLIT = 1, XCHG_HALF = 2 };
+enum { XCHG_FULL = 0, XCHG_SPLIT = 1, XCHG_HALF = 2, XCHG_LANE = 3 };
 
 
 template <int... Rs>
@@ -81,7 +84,8 @@ struct KCfg {
     static constexpr int RSKEW = C_ == 1 ? 0 : (XCHG_ == XCHG_FULL ? 16 : 32) / C_;
     static constexpr int ROW_SPAN = N_ + (N_ >> PADSH) + RSKEW;
     static constexpr int SPAN = COLS_ ? (N_ * C_ + ((N_ * C_) >> PADSH)) : C_ * ROW_SPAN;
-    static constexpr int LDS_FLOATS = XCHG_ == XCHG_FULL ? 2 * SPAN : SPAN;
+    // the cross-lane kernels keep each transform inside one wave: no LDS
+    static constexpr int LDS_FLOATS = XCHG_ == XCHG_LANE ? 1 : XCHG_ == XCHG_FULL ? 2 * SPAN : SPAN;
     // Waves per SIMD the LDS allows (a CU has 4 SIMDs and 160 KiB of LDS),
     // capped at 4: asking the compiler for this occupancy keeps it from
     // spending registers the LDS limit would not let other waves use anyway,
@@ -94,6 +98,8 @@ struct KCfg {
     static_assert((N_ & (N_ - 1)) == 0 && (P_ & (P_ - 1)) == 0 && (C_ & (C_ - 1)) == 0, "powers of two");
     static_assert(THREADS <= 1024, "at most 1024 threads per workgroup");
     static_assert(LDS_FLOATS * 4 <= 160 * 1024, "gfx950 LDS is 160 KiB per workgroup");
+    static_assert(XCHG_ != XCHG_LANE || (N_ == 1024 && P_ == 16 && !COLS_ && !PERSIST_),
+                  "cross-lane exchanges: 1024-point rows, one transform per wave");
 };
 
 template <class... Ks>
@@ -327,6 +333,12 @@ __device__ __forceinline__ void run_fft(Radices<R1, Rs...>, float2 (&v)[K::P], i
     run_stages<K, INV, FIRST_X, 1, R1, Rs...>(v, t, c, tw, lds, none);
 }
 
+}  // namespace mi355fft
+
+#include "fft_lane.hpp"
+
+namespace mi355fft {
+
 // Blocks are dispatched round-robin over the 8 XCDs.  Strips whose pieces
 // share a 128-byte line should run on one XCD, so the line meets them in one
 // L2.  Two block -> strip maps (xcd_remap):
@@ -400,6 +412,34 @@ __device__ __forceinline__ void store_points(const float2 (&v)[K::P], void *__re
         static_for<0, K::P>([&](auto ic) {
             constexpr int i = decltype(ic)::value;
             const long long pos = t + K::T * i;
+            Store<ST>::template store<NT>(dst + pos * a.out_stride, v[i]);
+        });
+    }
+}
+
+// Store of a cross-lane 1024-point kernel: register i of lane t holds point
+// lane_base_1024(t) + lane_reg_pos_1024<i>() (each register still covers 64
+// consecutive points, in another lane order).
+template <class K, int ST, bool NT>
+__device__ __forceinline__ void store_points_lane(const float2 (&v)[K::P], void *__restrict__ out, long long blk,
+                                                  int c, int t, const KArgs &a) {
+    constexpr int EL = Store<ST>::BYTES;
+    const int base = lane_base_1024(t);
+    if (!a.wide) {
+        char *b = reinterpret_cast<char *>(out) + blk * K::C * a.out_dist * EL;
+        const rsrc_t r = make_rsrc(b, a.out_span);
+        const unsigned lane = (unsigned)((c * a.out_dist + (long long)base * a.out_stride) * EL);
+        static_for<0, K::P>([&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            const unsigned soff = (unsigned)((long long)lane_reg_pos_1024<i>() * a.out_stride * EL);
+            Store<ST>::template store<NT>(r, lane, soff, v[i]);
+        });
+    } else {
+        using T = typename Store<ST>::T;
+        T *dst = reinterpret_cast<T *>(out) + (blk * K::C + c) * a.out_dist;
+        static_for<0, K::P>([&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            const long long pos = base + lane_reg_pos_1024<i>();
             Store<ST>::template store<NT>(dst + pos * a.out_stride, v[i]);
         });
     }
@@ -650,7 +690,12 @@ __device__ __forceinline__ void transform(float2 (&v)[K::P], int t, int c, const
                                           const float2 *__restrict__ spec, float scale, float *lds,
                                           int spec_off = 0, int spec_shift = 0) {
     constexpr bool MF = EPI == EPI_MATCHED || EPI == EPI_MATCHED_Y;
-    run_fft<K, INV, FIRST_X>(typename K::Rad{}, v, t, c, tw, lds);
+    if constexpr (K::XCHG == XCHG_LANE) {
+        static_assert(EPI == EPI_NONE, "the cross-lane kernels run plain transforms");
+        lane_fft_1024<K, INV>(v, t, tw);
+    } else {
+        run_fft<K, INV, FIRST_X>(typename K::Rad{}, v, t, c, tw, lds);
+    }
     if constexpr (MF) {
         // X[k] * conj(H[k]) * scale, k = t + T*i, then the inverse transform.
         // The scheduling fences keep the two transforms' register lifetimes
@@ -721,9 +766,11 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
     // one: 2.5-2.8% on the FP16 row transforms, while the memory-bound FP32
     // kernels lose up to 10% with it.
     constexpr bool PRIO = IN_ST == 1 && OUT_ST == 1;
-    if (blockIdx.y) {  // several independent problems along the grid's second axis
-        in = reinterpret_cast<const char *>(in) + (long long)blockIdx.y * a.outer_in_dist * Store<IN_ST>::BYTES;
-        out = reinterpret_cast<char *>(out) + (long long)blockIdx.y * a.outer_out_dist * Store<OUT_ST>::BYTES;
+    if (blockIdx.y | blockIdx.z) {  // independent problems along the grid's second and third axes
+        const long long in_off = (long long)blockIdx.y * a.outer_in_dist + (long long)blockIdx.z * a.outer2_dist;
+        const long long out_off = (long long)blockIdx.y * a.outer_out_dist + (long long)blockIdx.z * a.outer2_dist;
+        in = reinterpret_cast<const char *>(in) + in_off * Store<IN_ST>::BYTES;
+        out = reinterpret_cast<char *>(out) + out_off * Store<OUT_ST>::BYTES;
     }
     const int tid = threadIdx.x;
     const int c = K::COLS ? (tid & (K::C - 1)) : (tid >> K::LOG_T);
@@ -776,6 +823,11 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
             auto look = [&](int m) { return cmul(lo[m & mask], hi[m >> a.aux]); };
             float2 cf[4];
             cf[0] = look(n2 * t);
+            if constexpr (EPI != EPI_MATCHED_Y) {
+                // this pass's share 2^-s of the plan's output scale, folded
+                // into the factors (exact: a power of two)
+                cf[0] = make_float2(cf[0].x * a.scale, cf[0].y * a.scale);
+            }
             const float2 w1 = look(n2 * K::T);
             const float2 w2 = cmul(w1, w1);
             cf[1] = cmul(cf[0], w1);
@@ -807,7 +859,11 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
             store_remapped<K, OUT_ST>(v, out, blk, c, t, a, lds);
         } else {
             if constexpr (PRIO) __builtin_amdgcn_s_setprio(3);
-            if (valid) store_points<K, OUT_ST, NT>(v, out, blk, c, t, a);
+            if constexpr (K::XCHG == XCHG_LANE) {
+                if (valid) store_points_lane<K, OUT_ST, NT>(v, out, blk, c, t, a);
+            } else {
+                if (valid) store_points<K, OUT_ST, NT>(v, out, blk, c, t, a);
+            }
             if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
         }
     } else {
@@ -854,9 +910,11 @@ hipError_t launch_one(const void *in, void *out, const float2 *tw, const float2 
         if (blocks > resident.load(std::memory_order_relaxed)) blocks = resident.load(std::memory_order_relaxed);
     }
     const unsigned outer = a.outer > 1 ? (unsigned)a.outer : 1u;
-    if (outer > 1 && K::PERSIST) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(kern, dim3((unsigned)blocks, outer), dim3(K::THREADS), 0, stream, in, out, tw, spec, a);
-    return hipGetLastError();
+    const unsigned outer2 = a.outer2 > 1 ? (unsigned)a.outer2 : 1u;
+    if ((outer > 1 || outer2 > 1) && K::PERSIST) return hipErrorInvalidValue;
+    if (outer > 65535 || outer2 > 65535) return hipErrorInvalidValue;
+    return launch_kernel(kern, dim3((unsigned)blocks, outer, outer2), dim3(K::THREADS), stream, in, out, tw, spec,
+                         a);
 }
 
 }  // namespace mi355fft

@@ -4,7 +4,29 @@
 
 #include <hip/hip_runtime.h>
 
+#include <tuple>
+#include <utility>
+
 namespace mi355fft {
+
+// Launches a kernel and returns the status of this launch alone.  Reading
+// hipGetLastError after a triple-chevron launch would also return (and clear)
+// an earlier, unrelated error of the calling thread.  The arguments are
+// converted to the kernel's parameter types and passed by address.
+template <class... Params, class... Args, size_t... I>
+hipError_t launch_kernel_impl(void (*kern)(Params...), dim3 grid, dim3 block, hipStream_t s,
+                              std::index_sequence<I...>, Args &&...args) {
+    std::tuple<Params...> vals(std::forward<Args>(args)...);
+    void *ptrs[sizeof...(Params) > 0 ? sizeof...(Params) : 1] = {static_cast<void *>(&std::get<I>(vals))...};
+    return hipLaunchKernel(reinterpret_cast<const void *>(kern), grid, block, ptrs, 0, s);
+}
+
+template <class... Params, class... Args>
+hipError_t launch_kernel(void (*kern)(Params...), dim3 grid, dim3 block, hipStream_t s, Args &&...args) {
+    static_assert(sizeof...(Params) == sizeof...(Args), "one argument per kernel parameter");
+    return launch_kernel_impl(kern, grid, block, s, std::index_sequence_for<Params...>{},
+                              std::forward<Args>(args)...);
+}
 
 // Kernel families: contiguous rows, strided column strips, and the
 // migration-correction pass (row-mapped kernels over the transposed
@@ -85,6 +107,8 @@ struct KArgs {
     long long outer_in_dist;   // elements between the problems of blockIdx.y (input)
     long long outer_out_dist;  // elements between the problems of blockIdx.y (output)
     int outer;                 // problems along blockIdx.y (0 or 1: one)
+    int outer2;                // problems along blockIdx.z (0 or 1: one), each outer2_dist
+    long long outer2_dist;     // elements apart in both input and output
     int aux;                   // EPI_TWIDDLE(_Y): log2 of the low twiddle table's length
     // EPI_TWIDDLE with a row permutation: transform m of the batch is written
     // as row ((m mod 2^perm_b) << perm_a) | (m >> perm_b) (0, 0: row m)

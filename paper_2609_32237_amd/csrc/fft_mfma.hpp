@@ -223,13 +223,8 @@ hipError_t launch_mfma(int inv, const void *in, void *out, const float2 *tw, con
     const mf_half8 *am = reinterpret_cast<const mf_half8 *>(amat);
     if (a.batch <= 0 || a.batch > 0x7fffffffLL || a.stride != 1) return hipErrorInvalidValue;
     if (a.in_dist < M::N || a.out_dist < M::N) return hipErrorInvalidValue;
-    if (inv)
-        hipLaunchKernelGGL((fft_mfma_kernel<M, true>), dim3((unsigned)a.batch), dim3(M::THREADS), 0, s, in, out, tw,
-                           am, a);
-    else
-        hipLaunchKernelGGL((fft_mfma_kernel<M, false>), dim3((unsigned)a.batch), dim3(M::THREADS), 0, s, in, out, tw,
-                           am, a);
-    return hipGetLastError();
+    return launch_kernel(inv ? fft_mfma_kernel<M, true> : fft_mfma_kernel<M, false>, dim3((unsigned)a.batch),
+                         dim3(M::THREADS), s, in, out, tw, am, a);
 }
 
 }  // namespace mi355fft

@@ -49,10 +49,9 @@ hipError_t launch_rd_tables(long long n_az, long long n_rg, double wavelength, d
     long long most = n_az > n_rg ? n_az : n_rg;
     if (most < (kRcmcSub + 1) * kRcmcTaps) most = (kRcmcSub + 1) * kRcmcTaps;
     const unsigned blocks = (unsigned)((most + 255) / 256);
-    hipLaunchKernelGGL(rd_tables_kernel, dim3(blocks), dim3(256), 0, s, n_az, n_rg, wavelength, speed, prf,
-                       range_bin, r_near, interp_src, reinterpret_cast<float4 *>(base + l.rows),
-                       reinterpret_cast<float2 *>(base + l.cols), reinterpret_cast<float2 *>(base + l.interp));
-    return hipGetLastError();
+    return launch_kernel(rd_tables_kernel, dim3(blocks), dim3(256), s, n_az, n_rg, wavelength, speed, prf, range_bin,
+                         r_near, interp_src, reinterpret_cast<float4 *>(base + l.rows),
+                         reinterpret_cast<float2 *>(base + l.cols), reinterpret_cast<float2 *>(base + l.interp));
 }
 
 }  // namespace mi355fft

@@ -5,6 +5,7 @@
 // kernel launch per call; nothing here synchronises.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstdlib>
@@ -23,6 +24,11 @@ struct fft_plan {
     int64_t n, batch, stride, dist;
     int storage, dir, device, layout, xcd_remap, variant;
     float scale;  // output scale 2^-s (exact)
+    // The split forms spread that scale over their passes so that no stored
+    // intermediate grows past the final bound (FP16 storage): 2^-s1 in the
+    // first pass, 2^-s2 in the middle pass of three, the rest in the last.
+    // Powers of two are exact, so FP32 results are those of one final scale.
+    float scale1, scale2, scale_last;
     int mfma;     // radix-16 butterflies on the matrix cores (FP16 storage)
     const void *amat;
     const float2 *tw;
@@ -71,6 +77,15 @@ int map_hip(hipError_t e) {
 std::mutex g_tw_mutex;
 std::map<std::pair<int, int64_t>, float2 *> g_tw;
 
+void host_twiddles(int64_t n, std::vector<float2> &host) {
+    host.resize((size_t)n);
+    const double two_pi = 6.283185307179586476925286766559;
+    for (int64_t m = 0; m < n; ++m) {
+        const double ang = two_pi * ((double)m / (double)n);
+        host[(size_t)m] = make_float2((float)std::cos(ang), (float)-std::sin(ang));
+    }
+}
+
 int get_twiddles(int device, int64_t n, const float2 **out) {
     std::lock_guard<std::mutex> lock(g_tw_mutex);
     auto it = g_tw.find({device, n});
@@ -79,12 +94,8 @@ int get_twiddles(int device, int64_t n, const float2 **out) {
         return FFT_OK;
     }
     if (fail_alloc_hook()) return FFT_ENOMEM;
-    std::vector<float2> host((size_t)n);
-    const double two_pi = 6.283185307179586476925286766559;
-    for (int64_t m = 0; m < n; ++m) {
-        const double ang = two_pi * ((double)m / (double)n);
-        host[(size_t)m] = make_float2((float)std::cos(ang), (float)-std::sin(ang));
-    }
+    std::vector<float2> host;
+    host_twiddles(n, host);
     float2 *dev = nullptr;
     hipError_t e = hipMalloc((void **)&dev, sizeof(float2) * (size_t)n);
     if (e != hipSuccess) return map_hip(e);
@@ -172,15 +183,9 @@ int get_interp(int device, const float2 **out) {
 std::mutex g_ftab_mutex;
 std::map<std::pair<int, int64_t>, float2 *> g_ftab;
 
-int get_fourstep_table(int device, int64_t n, int log2s, const float2 **out) {
-    std::lock_guard<std::mutex> lock(g_ftab_mutex);
-    auto it = g_ftab.find({device, n});
-    if (it != g_ftab.end()) {
-        *out = it->second;
-        return FFT_OK;
-    }
+void host_fourstep_table(int64_t n, int log2s, std::vector<float2> &host) {
     const int64_t s = int64_t(1) << log2s, h = n / s;
-    std::vector<float2> host((size_t)(s + h));
+    host.resize((size_t)(s + h));
     const double two_pi = 6.283185307179586476925286766559;
     for (int64_t m = 0; m < s; ++m) {
         const double ang = two_pi * ((double)m / (double)n);
@@ -190,6 +195,17 @@ int get_fourstep_table(int device, int64_t n, int log2s, const float2 **out) {
         const double ang = two_pi * ((double)(m * s) / (double)n);
         host[(size_t)(s + m)] = make_float2((float)std::cos(ang), (float)-std::sin(ang));
     }
+}
+
+int get_fourstep_table(int device, int64_t n, int log2s, const float2 **out) {
+    std::lock_guard<std::mutex> lock(g_ftab_mutex);
+    auto it = g_ftab.find({device, n});
+    if (it != g_ftab.end()) {
+        *out = it->second;
+        return FFT_OK;
+    }
+    std::vector<float2> host;
+    host_fourstep_table(n, log2s, host);
     float2 *dev = nullptr;
     hipError_t e = hipMalloc((void **)&dev, sizeof(float2) * host.size());
     if (e != hipSuccess) return map_hip(e);
@@ -443,6 +459,13 @@ int fft_plan_create_ex(int64_t n, int64_t batch, int64_t stride, int64_t dist, i
     fft_plan *p = new (std::nothrow) fft_plan;
     if (!p) return FFT_ENOMEM;
     p->scale = std::ldexp(1.0f, -scale_log2);
+    {
+        const int s1 = split ? std::min(scale_log2, ilog2(n1)) : 0;
+        const int s2 = three ? std::min(scale_log2 - s1, ilog2(na)) : 0;
+        p->scale1 = std::ldexp(1.0f, -s1);
+        p->scale2 = std::ldexp(1.0f, -s2);
+        p->scale_last = std::ldexp(1.0f, -(scale_log2 - s1 - s2));
+    }
     p->mfma = mfma;
     p->amat = amat;
     p->n1 = n1;
@@ -496,7 +519,7 @@ static int execute_three_pass(const fft_plan *plan, const void *in, void *out, i
         const int64_t nbat = plan->batch - b0 < 65535 ? plan->batch - b0 : 65535;
         const char *pin = (const char *)in + (size_t)(b0 * plan->dist) * el;
         char *pout = (char *)out + (size_t)(b0 * plan->dist) * el;
-        KArgs a1{n2, n2, 1, n1, 1.0f, strip_map(n2 * (int64_t)el)};
+        KArgs a1{n2, n2, 1, n1, plan->scale1, strip_map(n2 * (int64_t)el)};
         a1.out_stride = 1;
         a1.outer = (int)nbat;
         a1.outer_in_dist = a1.outer_out_dist = plan->dist;
@@ -507,20 +530,25 @@ static int execute_three_pass(const fft_plan *plan, const void *in, void *out, i
                                   mi355fft::EPI_TWIDDLE, pin, pout, plan->tw1, plan->ftab, a1, stream);
         if (e != hipSuccess) return map_hip(e);
     }
-    // passes 2 and 3 use the grid's second axis for the groups: one launch
-    // per problem
-    for (int64_t b = 0; b < plan->batch; ++b) {
-        char *p = (char *)out + (size_t)(b * plan->dist) * el;
-        KArgs a2{n1, n1, 1, 1, 1.0f, strip_map(n1 * (int64_t)el)};
+    // passes 2 and 3 use the grid's second axis for the groups and its third
+    // for the problems (at most 65535 per launch)
+    for (int64_t b0 = 0; b0 < plan->batch; b0 += 65535) {
+        const int64_t nbat = plan->batch - b0 < 65535 ? plan->batch - b0 : 65535;
+        char *p = (char *)out + (size_t)(b0 * plan->dist) * el;
+        KArgs a2{n1, n1, 1, 1, plan->scale2, strip_map(n1 * (int64_t)el)};
         a2.outer = (int)nb;
         a2.outer_in_dist = a2.outer_out_dist = na * n1;
+        a2.outer2 = (int)nbat;
+        a2.outer2_dist = plan->dist;
         a2.aux = plan->log2s2;
         hipError_t e = launch_fft(na, plan->va, mi355fft::LAYOUT_COLS, plan->storage, plan->storage, inv,
                                   mi355fft::EPI_TWIDDLE_Y, p, p, plan->twa, plan->ftab2, a2, stream);
         if (e != hipSuccess) return map_hip(e);
-        KArgs a3{n1, na * n1, 1, 1, plan->scale, strip_map(na * n1 * (int64_t)el)};
+        KArgs a3{n1, na * n1, 1, 1, plan->scale_last, strip_map(na * n1 * (int64_t)el)};
         a3.outer = (int)na;
         a3.outer_in_dist = a3.outer_out_dist = n1;
+        a3.outer2 = (int)nbat;
+        a3.outer2_dist = plan->dist;
         e = launch_fft(nb, plan->vb, mi355fft::LAYOUT_COLS, plan->storage, plan->storage, inv, mi355fft::EPI_NONE,
                        p, p, plan->twb, nullptr, a3, stream);
         if (e != hipSuccess) return map_hip(e);
@@ -538,7 +566,7 @@ static int execute_three_pass(const fft_plan *plan, const void *in, void *out, i
 static int execute_column_split(const fft_plan *plan, const void *in, void *out, int inv, hipStream_t stream) {
     const int64_t n1 = plan->n1, n2 = plan->n2, s = plan->stride;
     const size_t el = plan->storage == FFT_STORAGE_FP32 ? 8 : 4;
-    KArgs a1{plan->batch, n2 * s, 1, 1, 1.0f, strip_map(n2 * s * (int64_t)el)};
+    KArgs a1{plan->batch, n2 * s, 1, 1, plan->scale1, strip_map(n2 * s * (int64_t)el)};
     a1.out_stride = s;
     a1.outer = (int)n2;
     a1.outer_in_dist = s;
@@ -547,7 +575,7 @@ static int execute_column_split(const fft_plan *plan, const void *in, void *out,
     hipError_t e = launch_fft(n1, plan->v1, mi355fft::LAYOUT_COLS, plan->storage, plan->storage, inv,
                               mi355fft::EPI_TWIDDLE_Y, in, out, plan->tw1, plan->ftab, a1, stream);
     if (e != hipSuccess) return map_hip(e);
-    KArgs a2{plan->batch, n1 * s, 1, 1, plan->scale, strip_map(n1 * s * (int64_t)el)};
+    KArgs a2{plan->batch, n1 * s, 1, 1, plan->scale_last, strip_map(n1 * s * (int64_t)el)};
     a2.outer = (int)n1;
     a2.outer_in_dist = a2.outer_out_dist = s;
     e = launch_fft(n2, plan->v2, mi355fft::LAYOUT_COLS, plan->storage, plan->storage, inv, mi355fft::EPI_NONE, out,
@@ -559,6 +587,14 @@ int fft_execute(const fft_plan *plan, const void *in, void *out, hipStream_t str
     if (!plan || !in || !out) return FFT_EINVAL;
     const size_t el = plan->storage == FFT_STORAGE_FP32 ? 8 : 4;
     if (!aligned(in, el) || !aligned(out, el)) return FFT_EALIGN;
+    // in place, or two disjoint extents (the plan bounded the extent by 2^40 elements)
+    const size_t extent = (size_t)((plan->batch - 1) * plan->dist + (plan->n - 1) * plan->stride + 1) * el;
+    if (in != out && overlaps(in, extent, out, extent)) return FFT_EINVAL;
+    // the plan's tables live on the device it was created on
+    int device = 0;
+    const hipError_t de = hipGetDevice(&device);
+    if (de != hipSuccess) return map_hip(de);
+    if (device != plan->device) return FFT_EINVAL;
     if (plan->colsplit && in != out) return execute_column_split(plan, in, out, plan->dir == FFT_INVERSE, stream);
     if (plan->n1 && !plan->colsplit && (plan->n > kMaxN || in != out)) {
         // four-step (Section VI's two-pass transform for lengths beyond the
@@ -575,7 +611,7 @@ int fft_execute(const fft_plan *plan, const void *in, void *out, hipStream_t str
             const int64_t nb = plan->batch - b0 < 65535 ? plan->batch - b0 : 65535;
             const char *pin = (const char *)in + (size_t)(b0 * plan->dist) * el;
             char *pout = (char *)out + (size_t)(b0 * plan->dist) * el;
-            KArgs a1{n2, n2, 1, n1, 1.0f, strip_map(n2 * (int64_t)el)};
+            KArgs a1{n2, n2, 1, n1, plan->scale1, strip_map(n2 * (int64_t)el)};
             a1.out_stride = 1;
             a1.outer = (int)nb;
             a1.outer_in_dist = a1.outer_out_dist = plan->dist;
@@ -583,7 +619,7 @@ int fft_execute(const fft_plan *plan, const void *in, void *out, hipStream_t str
             hipError_t e = launch_fft(n1, plan->v1, mi355fft::LAYOUT_COLS, plan->storage, plan->storage, inv,
                                       mi355fft::EPI_TWIDDLE, pin, pout, plan->tw1, plan->ftab, a1, stream);
             if (e != hipSuccess) return map_hip(e);
-            KArgs a2{n1, n1, 1, 1, plan->scale, strip_map(n1 * (int64_t)el)};
+            KArgs a2{n1, n1, 1, 1, plan->scale_last, strip_map(n1 * (int64_t)el)};
             a2.outer = (int)nb;
             a2.outer_in_dist = a2.outer_out_dist = plan->dist;
             e = launch_fft(n2, plan->v2, mi355fft::LAYOUT_COLS, plan->storage, plan->storage, inv,
@@ -636,20 +672,26 @@ static bool long_azimuth(int64_t n_az, int inter_storage) {
     return inter_storage == FFT_STORAGE_FP32 && (n_az == 8192 || n_az == 16384);
 }
 
-static int sar_long_azimuth(int64_t n_az, int64_t n_rg, const void *raw, void *out, void *mid, const float2 *h_rg,
-                     const float2 *h_az, const float2 *tw_rg, int vrow, int device, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// Device tables one SAR image needs: the twiddles of both axes and, for the
+// long-azimuth form, those of its 128-point and n2-point columns and the
+// two-level table of the azimuth length.
+struct SarTables {
+    const float2 *tw_rg, *tw_az, *tw1, *tw2, *ftab;
+};
+
+int sar_long_azimuth(int64_t n_az, int64_t n_rg, const void *raw, void *out, void *mid, const float2 *h_rg,
+                            const float2 *h_az, const SarTables &t, int vrow, hipStream_t stream) {
     using mi355fft::LAYOUT_COLS;
     const int64_t n1 = 128, n2 = n_az / n1;
-    const float2 *tw1 = nullptr, *tw2 = nullptr, *ftab = nullptr;
     const int log2s = (ilog2(n_az) + 1) / 2;
-    int rc = get_twiddles(device, n1, &tw1);
-    if (rc == FFT_OK) rc = get_twiddles(device, n2, &tw2);
-    if (rc == FFT_OK) rc = get_fourstep_table(device, n_az, log2s, &ftab);
-    if (rc != FFT_OK) return rc;
     // range pass into `out`
     const KArgs ar{n_az, 1, n_rg, n_rg, (float)(1.0 / (double)n_rg), 0};
     hipError_t e = launch_fft(n_rg, vrow, mi355fft::LAYOUT_ROWS, FFT_STORAGE_FP32, FFT_STORAGE_FP32, 0,
-                              mi355fft::EPI_MATCHED, raw, out, tw_rg, h_rg, ar, stream);
+                              mi355fft::EPI_MATCHED, raw, out, t.tw_rg, h_rg, ar, stream);
     if (e != hipSuccess) return map_hip(e);
     KArgs b1{n_rg, n2 * n_rg, 1, 1, 1.0f, strip_map(n2 * n_rg * 8)};
     b1.out_stride = n_rg;
@@ -657,50 +699,44 @@ static int sar_long_azimuth(int64_t n_az, int64_t n_rg, const void *raw, void *o
     b1.outer_in_dist = n_rg;
     b1.outer_out_dist = n1 * n_rg;
     b1.aux = log2s;
-    e = launch_fft(n1, -1, LAYOUT_COLS, FFT_STORAGE_FP32, FFT_STORAGE_FP32, 0, mi355fft::EPI_TWIDDLE_Y, out, mid, tw1,
-                   ftab, b1, stream);
+    e = launch_fft(n1, -1, LAYOUT_COLS, FFT_STORAGE_FP32, FFT_STORAGE_FP32, 0, mi355fft::EPI_TWIDDLE_Y, out, mid,
+                   t.tw1, t.ftab, b1, stream);
     if (e != hipSuccess) return map_hip(e);
     KArgs b2{n_rg, n1 * n_rg, 1, 1, (float)(1.0 / (double)n_az), strip_map(n1 * n_rg * 8)};
     b2.outer = (int)n1;
     b2.outer_in_dist = b2.outer_out_dist = n_rg;
     b2.aux = log2s;
     b2.spec_shift = ilog2(n1);
-    b2.tab2 = ftab;
-    e = launch_fft(n2, -1, LAYOUT_COLS, FFT_STORAGE_FP32, FFT_STORAGE_FP32, 0, mi355fft::EPI_MATCHED_Y, mid, mid, tw2,
-                   h_az, b2, stream);
+    b2.tab2 = t.ftab;
+    e = launch_fft(n2, -1, LAYOUT_COLS, FFT_STORAGE_FP32, FFT_STORAGE_FP32, 0, mi355fft::EPI_MATCHED_Y, mid, mid,
+                   t.tw2, h_az, b2, stream);
     if (e != hipSuccess) return map_hip(e);
     KArgs b3{n_rg, n_rg, 1, 1, 1.0f, strip_map(n_rg * 8)};
     b3.out_stride = n2 * n_rg;
     b3.outer = (int)n2;
     b3.outer_in_dist = n1 * n_rg;
     b3.outer_out_dist = n_rg;
-    e = launch_fft(n1, -1, LAYOUT_COLS, FFT_STORAGE_FP32, FFT_STORAGE_FP32, 1, mi355fft::EPI_NONE, mid, out, tw1,
+    e = launch_fft(n1, -1, LAYOUT_COLS, FFT_STORAGE_FP32, FFT_STORAGE_FP32, 1, mi355fft::EPI_NONE, mid, out, t.tw1,
                    nullptr, b3, stream);
     return map_hip(e);
 }
 
-int sar_form_image_ex(int64_t n_az, int64_t n_rg, int inter_storage, const void *raw, const void *range_ref,
-                      const void *az_ref, void *out, void *workspace, hipStream_t stream) {
-    if (!raw || !range_ref || !az_ref || !out || !workspace) return FFT_EINVAL;
+// Argument checks shared by both SAR entry points (no HIP call).
+int sar_check(int64_t n_az, int64_t n_rg, int inter_storage, const void *raw, const void *range_ref,
+                     const void *az_ref, const void *out) {
+    if (!raw || !range_ref || !az_ref || !out) return FFT_EINVAL;
     if (inter_storage != FFT_STORAGE_FP32 && inter_storage != FFT_STORAGE_FP16) return FFT_EINVAL;
     if (n_az < 1 || n_rg < 1) return FFT_EINVAL;
     if (!supported_n(n_az) || !supported_n(n_rg)) return FFT_EUNSUPPORTED;
-    if (!aligned(raw, 8) || !aligned(range_ref, 8) || !aligned(az_ref, 8) || !aligned(out, 8) ||
-        !aligned(workspace, 256))
-        return FFT_EALIGN;
+    if (!aligned(raw, 8) || !aligned(range_ref, 8) || !aligned(az_ref, 8) || !aligned(out, 8)) return FFT_EALIGN;
     const size_t img = (size_t)n_az * (size_t)n_rg * 8;
-    const size_t ws = sar_workspace_bytes(n_az, n_rg, inter_storage);
-    if (overlaps(out, img, raw, img) || overlaps(out, img, workspace, ws) || overlaps(raw, img, workspace, ws))
-        return FFT_EINVAL;
+    if (overlaps(out, img, raw, img)) return FFT_EINVAL;
+    return FFT_OK;
+}
 
-    int device = 0;
-    hipError_t e = hipGetDevice(&device);
-    if (e != hipSuccess) return map_hip(e);
-    const float2 *tw_rg = nullptr, *tw_az = nullptr;
-    int rc = get_twiddles(device, n_rg, &tw_rg);
-    if (rc == FFT_OK) rc = get_twiddles(device, n_az, &tw_az);
-    if (rc != FFT_OK) return rc;
-
+// The chain itself, on checked arguments, with its tables and workspace given.
+int sar_run(int64_t n_az, int64_t n_rg, int inter_storage, const void *raw, const void *range_ref,
+                   const void *az_ref, void *out, void *workspace, const SarTables &t, hipStream_t stream) {
     const int vrow = chosen_variant(n_rg, mi355fft::LAYOUT_ROWS);
     const int vcol = chosen_variant(n_az, mi355fft::LAYOUT_COLS);
     const int vref = chosen_variant(n_az, mi355fft::LAYOUT_ROWS);
@@ -713,6 +749,7 @@ int sar_form_image_ex(int64_t n_az, int64_t n_rg, int inter_storage, const void 
     using mi355fft::EPI_NONE;
     using mi355fft::LAYOUT_COLS;
     using mi355fft::LAYOUT_ROWS;
+    hipError_t e;
 
     // reference spectra H = FFT(ref) into the workspace; the passes multiply by
     // conj(H).  Equal lengths: one launch of two transforms (the input distance
@@ -720,32 +757,61 @@ int sar_form_image_ex(int64_t n_az, int64_t n_rg, int inter_storage, const void 
     if (n_rg == n_az) {
         const long long gap = ((const char *)az_ref - (const char *)range_ref) / (long long)sizeof(float2);
         const KArgs a{2, 1, gap, n_rg, 1.0f, 0};
-        e = launch_fft(n_rg, vrow, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, range_ref, h_rg, tw_rg, nullptr, a, stream);
+        e = launch_fft(n_rg, vrow, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, range_ref, h_rg, t.tw_rg, nullptr, a, stream);
         if (e != hipSuccess) return map_hip(e);
     } else {
         const KArgs a1{1, 1, n_rg, n_rg, 1.0f, 0};
-        e = launch_fft(n_rg, vrow, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, range_ref, h_rg, tw_rg, nullptr, a1, stream);
+        e = launch_fft(n_rg, vrow, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, range_ref, h_rg, t.tw_rg, nullptr, a1, stream);
         if (e != hipSuccess) return map_hip(e);
         const KArgs a2{1, 1, n_az, n_az, 1.0f, 0};
-        e = launch_fft(n_az, vref, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, az_ref, h_az, tw_az, nullptr, a2, stream);
+        e = launch_fft(n_az, vref, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, az_ref, h_az, t.tw_az, nullptr, a2, stream);
         if (e != hipSuccess) return map_hip(e);
     }
 
     if (long_azimuth(n_az, inter_storage)) {
-        return sar_long_azimuth(n_az, n_rg, raw, out, mid, h_rg, h_az, tw_rg, vrow, device, stream);
+        return sar_long_azimuth(n_az, n_rg, raw, out, mid, h_rg, h_az, t, vrow, stream);
     }
 
     // pass 1, rows (range): FFT, * conj(H_r) / n_rg, IFFT -> intermediate
     const KArgs ar{n_az, 1, n_rg, n_rg, (float)(1.0 / (double)n_rg), 0};
-    e = launch_fft(n_rg, vrow, LAYOUT_ROWS, FFT_STORAGE_FP32, inter_storage, 0, EPI_MATCHED, raw, mid, tw_rg, h_rg,
+    e = launch_fft(n_rg, vrow, LAYOUT_ROWS, FFT_STORAGE_FP32, inter_storage, 0, EPI_MATCHED, raw, mid, t.tw_rg, h_rg,
                    ar, stream);
     if (e != hipSuccess) return map_hip(e);
 
     // pass 2, columns (azimuth): FFT, / n_az * conj(H_a), IFFT -> image
     const KArgs ac{n_rg, n_rg, 1, 1, (float)(1.0 / (double)n_az), strip_map(n_rg * 8)};
-    e = launch_fft(n_az, vcol, LAYOUT_COLS, inter_storage, FFT_STORAGE_FP32, 0, EPI_MATCHED, mid, out, tw_az, h_az,
+    e = launch_fft(n_az, vcol, LAYOUT_COLS, inter_storage, FFT_STORAGE_FP32, 0, EPI_MATCHED, mid, out, t.tw_az, h_az,
                    ac, stream);
     return map_hip(e);
+}
+
+}  // namespace
+
+extern "C" {
+
+int sar_form_image_ex(int64_t n_az, int64_t n_rg, int inter_storage, const void *raw, const void *range_ref,
+                      const void *az_ref, void *out, void *workspace, hipStream_t stream) {
+    if (!workspace) return FFT_EINVAL;
+    int rc = sar_check(n_az, n_rg, inter_storage, raw, range_ref, az_ref, out);
+    if (rc != FFT_OK) return rc;
+    if (!aligned(workspace, 256)) return FFT_EALIGN;
+    const size_t img = (size_t)n_az * (size_t)n_rg * 8;
+    const size_t ws = sar_workspace_bytes(n_az, n_rg, inter_storage);
+    if (overlaps(out, img, workspace, ws) || overlaps(raw, img, workspace, ws)) return FFT_EINVAL;
+
+    int device = 0;
+    hipError_t e = hipGetDevice(&device);
+    if (e != hipSuccess) return map_hip(e);
+    SarTables t{};
+    rc = get_twiddles(device, n_rg, &t.tw_rg);
+    if (rc == FFT_OK) rc = get_twiddles(device, n_az, &t.tw_az);
+    if (rc == FFT_OK && long_azimuth(n_az, inter_storage)) {
+        rc = get_twiddles(device, 128, &t.tw1);
+        if (rc == FFT_OK) rc = get_twiddles(device, n_az / 128, &t.tw2);
+        if (rc == FFT_OK) rc = get_fourstep_table(device, n_az, (ilog2(n_az) + 1) / 2, &t.ftab);
+    }
+    if (rc != FFT_OK) return rc;
+    return sar_run(n_az, n_rg, inter_storage, raw, range_ref, az_ref, out, workspace, t, stream);
 }
 
 size_t sar_rd_workspace_bytes(int64_t n_az, int64_t n_rg, int inter_storage) {

@@ -180,17 +180,13 @@ def test_misaligned_pointer(api):
 
 # --------------------------------------------------------------------------
 # The benchmark workloads at full size, in the launch configuration the
-# benchmark times: sampled transforms against the oracle, Parseval on all.
+# benchmark times: every transform against the oracle, element by element
+# (the pass criterion is the per-transform error maximised over the batch,
+# Section III), with Parseval on every transform as an extra check.
 # --------------------------------------------------------------------------
 
 FULL = ["fft_n1024_b64_fp32", "fft_n4096_b32768_fp32", "fft_n8192_b16384_fp32", "fft_n16384_b8192_fp32",
         "fft_n16384_b16384_fp16"]
-
-
-def sample_rows(batch, k=48, seed=0):
-    rng = np.random.default_rng(seed)
-    rows = {0, 1, batch - 2, batch - 1} | set(rng.integers(0, batch, k).tolist())
-    return np.array(sorted(r for r in rows if 0 <= r < batch))
 
 
 def parseval_ratio(x, y):
@@ -198,6 +194,24 @@ def parseval_ratio(x, y):
     x, y = widen(x), widen(y)
     n = x.shape[-1]
     return (np.abs(y) ** 2).sum(-1) / (n * (np.abs(x) ** 2).sum(-1))
+
+
+def compare_all(x, y, sign, chunk_points=1 << 24):
+    """Per-transform relative L2 error of every transform of y against the
+    oracle on x, in chunks of about 2^24 points (256 MiB of complex128)."""
+    batch, n = x.shape[0], x.shape[1]
+    step = max(1, chunk_points // n)
+    err = np.empty(batch)
+    num = den = 0.0
+    for s in range(0, batch, step):
+        ref = oracle.fft(x[s:s + step], sign)
+        got = widen(y[s:s + step])
+        d = (np.abs(got - ref) ** 2).sum(-1)
+        r = (np.abs(ref) ** 2).sum(-1)
+        err[s:s + step] = np.sqrt(d / r)
+        num += d.sum()
+        den += r.sum()
+    return err, float(np.sqrt(num / den))
 
 
 @pytest.mark.parametrize("name", FULL)
@@ -214,29 +228,31 @@ def test_full_size_workload(api, name):
     plan.execute(xd, out)
     torch.cuda.synchronize()
     y = to_host(out)
-    rows = sample_rows(batch) if batch > 64 else np.arange(batch)
-    ref = oracle.fft(x[rows])
-    err = rel_rows(widen(y[rows]), ref)
-    log(f"  {name}: max rel {err.max():.3e}  SQNR {-20 * np.log10(err.max()):.1f} dB")
-    assert err.max() < TOL[storage]
+    err, glob = compare_all(x, y, -1)
+    worst = int(err.argmax())
+    log(f"  {name}: all {batch} transforms, max rel {err.max():.3e} (transform {worst}), "
+        f"median {np.median(err):.3e}, global {glob:.3e}, SQNR {-20 * np.log10(glob):.1f} dB")
+    assert err.max() < TOL[storage], (worst, err.max())
     # Parseval on every transform, in chunks
     tol = 2e-5 if storage == "fp32" else 5e-3
     for s in range(0, batch, 2048):
         r = parseval_ratio(x[s:s + 2048], y[s:s + 2048])
         assert np.abs(r - 1).max() < tol, (s, np.abs(r - 1).max())
     if name == "fft_n4096_b32768_fp32":
-        # round trip: inverse of the forward output equals N x
+        # round trip: inverse of the forward output equals N x, every transform
         inv = api.Plan(n, batch, 1, n, 0, 1)
         back = torch.empty_like(xd)
         inv.execute(out, back)
         torch.cuda.synchronize()
         b = to_host(back)
-        err = rel_rows(widen(b[rows]) / n, x[rows].astype(np.complex128))
-        log(f"  round trip max rel {err.max():.3e}")
-        assert err.max() < 1e-5
-        d = (b / np.float32(n) - x)
-        glob = np.sqrt((np.abs(d.astype(np.complex128)) ** 2).sum() / (np.abs(x.astype(np.complex128)) ** 2).sum())
-        assert glob < 1e-5
+        errs = np.empty(batch)
+        for s in range(0, batch, 4096):
+            errs[s:s + 4096] = rel_rows(widen(b[s:s + 4096]) / n, x[s:s + 4096].astype(np.complex128))
+        log(f"  round trip: max rel {errs.max():.3e}")
+        assert errs.max() < 1e-5
+        # the inverse itself against the oracle on the forward output, every transform
+        e_inv, _ = compare_all(y, b, 1)
+        assert e_inv.max() < 1e-5, e_inv.max()
         inv.close()
     plan.close()
 
