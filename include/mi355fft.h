@@ -238,6 +238,32 @@ int sar_form_image(const void *raw, const void *range_ref, const void *az_ref, v
                    hipStream_t stream);
 
 /*
+ * sar_form_image_noalloc -- sar_form_image_ex without a workspace argument,
+ * for callers that cannot allocate device memory: code under HIP graph
+ * capture (after the first call on the device), tight serving loops,
+ * harnesses that forbid hipMalloc.
+ *
+ * The workspace (both reference spectra and the intermediate image) and the
+ * twiddle tables live in one fixed device array of the library, 129 MiB on
+ * each device, held from the loading of the library's device code until the
+ * process ends; no call allocates or frees device memory.  The intermediate
+ * must fit it: n_az * n_rg * (8 with FP32, 4 with FP16 intermediates) at most
+ * 128 MiB (4096 x 4096 with FP32 intermediates, 8192 x 4096 with FP16), else
+ * FFT_EUNSUPPORTED, returned before any HIP call.  The first call on a device
+ * looks up the array's address there and copies the tables in with a
+ * synchronous hipMemcpy (so it must not be made under stream capture); later
+ * calls only launch kernels on `stream`.
+ * Every call on one device uses that device's one array: calls that overlap in
+ * time on one device (from several threads or streams) race.  The array keeps
+ * the last call's contents; nothing in it needs to start at zero, since each
+ * call writes every part of it that it reads.
+ * Other arguments, the computation and the other errors are those of
+ * sar_form_image_ex.
+ */
+int sar_form_image_noalloc(int64_t n_az, int64_t n_rg, int inter_storage, const void *raw,
+                           const void *range_ref, const void *az_ref, void *out, hipStream_t stream);
+
+/*
  * Acquisition geometry of a broadside stripmap echo (Section X's scene: an
  * L-band platform flying straight at constant speed, zero squint).
  */

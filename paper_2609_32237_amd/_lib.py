@@ -29,7 +29,7 @@ FFT_FLAG_FP16_EXCHANGE = 1
 FFT_FLAG_MATRIX_UNITS = 2
 
 EXPORTS = ("fft_plan_create", "fft_plan_create_ex", "fft_execute", "fft_plan_destroy", "sar_workspace_bytes",
-           "sar_form_image_ex", "sar_form_image", "sar_rd_workspace_bytes",
+           "sar_form_image_ex", "sar_form_image", "sar_form_image_noalloc", "sar_rd_workspace_bytes",
            "sar_rd_form_image", "fft_strerror")
 
 
@@ -60,6 +60,8 @@ lib.sar_form_image_ex.argtypes = [_i64, _i64, _int, _vp, _vp, _vp, _vp, _vp, _vp
 lib.sar_form_image_ex.restype = _int
 lib.sar_form_image.argtypes = [_vp, _vp, _vp, _vp, _vp]
 lib.sar_form_image.restype = _int
+lib.sar_form_image_noalloc.argtypes = [_i64, _i64, _int, _vp, _vp, _vp, _vp, _vp]
+lib.sar_form_image_noalloc.restype = _int
 lib.sar_rd_workspace_bytes.argtypes = [_i64, _i64, _int]
 lib.sar_rd_workspace_bytes.restype = ctypes.c_size_t
 lib.sar_rd_form_image.argtypes = [_i64, _i64, _int, ctypes.POINTER(SarGeometry), _vp, _vp, _vp, _vp, _vp]
@@ -120,6 +122,13 @@ def sar_form_image_ex(n_az: int, n_rg: int, inter_storage: int, raw: int, range_
 
 def sar_form_image(raw: int, range_ref: int, az_ref: int, out: int, stream: int = 0) -> None:
     _check(lib.sar_form_image(raw, range_ref, az_ref, out, stream), "sar_form_image")
+
+
+def sar_form_image_noalloc(n_az: int, n_rg: int, inter_storage: int, raw: int, range_ref: int, az_ref: int,
+                           out: int, stream: int = 0) -> None:
+    """sar_form_image_ex with the library's fixed device array as workspace."""
+    _check(lib.sar_form_image_noalloc(n_az, n_rg, inter_storage, raw, range_ref, az_ref, out, stream),
+           "sar_form_image_noalloc")
 
 
 def sar_rd_workspace_bytes(n_az: int, n_rg: int, inter_storage: int) -> int:

@@ -87,6 +87,16 @@ __host__ __device__ constexpr RdTablesLayout rd_tables_layout(long long n_az, lo
                               round_up_256((long long)(kRcmcSub + 1) * kRcmcTaps * 8)};
 }
 
+// The allocation-free SAR entry point keeps its tables and workspace in one
+// fixed device array per device (noalloc.hip), of kNoallocScratchBytes:
+// room for the twiddle tables, both reference spectra and an intermediate
+// image of at most kNoallocMaxImageBytes (the 4096 x 4096 image with FP32
+// intermediates).  noalloc_scratch returns the current device's copy of it;
+// the address is looked up once per device and kept.
+constexpr size_t kNoallocMaxImageBytes = size_t(128) << 20;
+constexpr size_t kNoallocScratchBytes = kNoallocMaxImageBytes + (size_t(1) << 20);
+hipError_t noalloc_scratch(int device, void **ptr);
+
 // Fills the range-Doppler tables (double-precision arithmetic on the device,
 // rounded once to FP32 or split into FP32 hi + lo pairs).
 hipError_t launch_rd_tables(long long n_az, long long n_rg, double wavelength, double speed, double prf,

@@ -785,6 +785,55 @@ int sar_run(int64_t n_az, int64_t n_rg, int inter_storage, const void *raw, cons
     return map_hip(e);
 }
 
+// The allocation-free SAR entry point's fixed device array (noalloc.hip):
+// the twiddle tables of every length 64 ... 16384 and the two-level tables of
+// 8192 and 16384, filled once per device, then the chain's workspace.
+constexpr size_t kNaTwBytes = (size_t)(2 * 16384 - 64) * sizeof(float2);  // lengths 64 .. 16384
+constexpr size_t kNaFtabOffset = kNaTwBytes;
+constexpr size_t kNaFtabBytes = (size_t)(192 + 256) * sizeof(float2);  // 8192: 128 + 64; 16384: 128 + 128
+constexpr size_t kNaWorkspaceOffset = mi355fft::round_up_256(kNaFtabOffset + kNaFtabBytes);
+static_assert(kNaWorkspaceOffset + 2 * 16384 * sizeof(float2) + mi355fft::kNoallocMaxImageBytes <=
+                  mi355fft::kNoallocScratchBytes,
+              "the fixed array holds the tables, both spectra and the largest intermediate");
+
+size_t na_tw_offset(int64_t n) { return (size_t)(n - 64) * sizeof(float2); }  // 64 + 128 + ... + n/2 = n - 64
+size_t na_ftab_offset(int64_t n) { return kNaFtabOffset + (n == 8192 ? 0 : 192 * sizeof(float2)); }
+
+std::mutex g_na_mutex;
+std::map<int, char *> g_na;  // device -> its array, tables filled
+
+// This device's copy of the array with its tables filled: the array's address
+// (looked up once per device in noalloc.hip) and, on the first call on the
+// device, the tables copied in from the host (the same double-precision
+// tables the plans use).
+int noalloc_base(int device, char **base) {
+    std::lock_guard<std::mutex> lock(g_na_mutex);
+    auto it = g_na.find(device);
+    if (it != g_na.end()) {
+        *base = it->second;
+        return FFT_OK;
+    }
+    void *p = nullptr;
+    hipError_t e = mi355fft::noalloc_scratch(device, &p);
+    if (e != hipSuccess) return map_hip(e);
+    char *b = static_cast<char *>(p);
+    std::vector<float2> host, all;
+    for (int64_t n = 64; n <= 16384; n *= 2) {
+        host_twiddles(n, host);
+        all.insert(all.end(), host.begin(), host.end());
+    }
+    for (int64_t n : {int64_t(8192), int64_t(16384)}) {
+        host_fourstep_table(n, (ilog2(n) + 1) / 2, host);
+        all.insert(all.end(), host.begin(), host.end());
+    }
+    if (all.size() * sizeof(float2) != kNaTwBytes + kNaFtabBytes) return FFT_EINVAL;  // layout mismatch
+    e = hipMemcpy(b, all.data(), all.size() * sizeof(float2), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return map_hip(e);
+    g_na[device] = b;
+    *base = b;
+    return FFT_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -812,6 +861,32 @@ int sar_form_image_ex(int64_t n_az, int64_t n_rg, int inter_storage, const void 
     }
     if (rc != FFT_OK) return rc;
     return sar_run(n_az, n_rg, inter_storage, raw, range_ref, az_ref, out, workspace, t, stream);
+}
+
+int sar_form_image_noalloc(int64_t n_az, int64_t n_rg, int inter_storage, const void *raw, const void *range_ref,
+                           const void *az_ref, void *out, hipStream_t stream) {
+    int rc = sar_check(n_az, n_rg, inter_storage, raw, range_ref, az_ref, out);
+    if (rc != FFT_OK) return rc;
+    const size_t el = inter_storage == FFT_STORAGE_FP32 ? 8 : 4;
+    if ((size_t)n_az * (size_t)n_rg * el > mi355fft::kNoallocMaxImageBytes) return FFT_EUNSUPPORTED;
+    int device = 0;
+    hipError_t e = hipGetDevice(&device);
+    if (e != hipSuccess) return map_hip(e);
+    char *base = nullptr;
+    rc = noalloc_base(device, &base);
+    if (rc != FFT_OK) return rc;
+    void *ws = base + kNaWorkspaceOffset;
+    const size_t img = (size_t)n_az * (size_t)n_rg * 8;
+    const size_t wsb = sar_workspace_bytes(n_az, n_rg, inter_storage);
+    if (overlaps(out, img, ws, wsb) || overlaps(raw, img, ws, wsb)) return FFT_EINVAL;
+    auto tw = [&](int64_t n) { return reinterpret_cast<const float2 *>(base + na_tw_offset(n)); };
+    SarTables t{tw(n_rg), tw(n_az), nullptr, nullptr, nullptr};
+    if (long_azimuth(n_az, inter_storage)) {
+        t.tw1 = tw(128);
+        t.tw2 = tw(n_az / 128);
+        t.ftab = reinterpret_cast<const float2 *>(base + na_ftab_offset(n_az));
+    }
+    return sar_run(n_az, n_rg, inter_storage, raw, range_ref, az_ref, out, ws, t, stream);
 }
 
 size_t sar_rd_workspace_bytes(int64_t n_az, int64_t n_rg, int inter_storage) {

@@ -31,7 +31,7 @@ def declared_functions():
 def test_header_declares_the_abi():
     assert declared_functions() == sorted(
         ["fft_plan_create", "fft_plan_create_ex", "fft_execute", "fft_plan_destroy", "sar_workspace_bytes", "sar_form_image_ex",
-         "sar_form_image", "sar_rd_workspace_bytes", "sar_rd_form_image", "fft_strerror"])
+         "sar_form_image", "sar_form_image_noalloc", "sar_rd_workspace_bytes", "sar_rd_form_image", "fft_strerror"])
 
 
 def test_library_exports_every_declared_symbol(L):
@@ -109,6 +109,22 @@ def test_sar_argument_errors(L):
     # out overlapping raw
     assert f(4096, 4096, 0, 1 << 30, ok, ok, (1 << 30) + 4096, 1 << 40, None) == L.FFT_EINVAL
     assert L.lib.sar_form_image(None, ok, ok, ok, None) == L.FFT_EINVAL
+
+
+def test_sar_noalloc_argument_errors(L):
+    """Every argument error, and an intermediate beyond the fixed array's
+    128 MiB, comes back before any HIP call."""
+    f = L.lib.sar_form_image_noalloc
+    ok = 1 << 20
+    assert f(4096, 4096, 0, None, ok, ok, ok, None) == L.FFT_EINVAL
+    assert f(4096, 4096, 3, ok, ok, ok, 1 << 40, None) == L.FFT_EINVAL
+    assert f(4000, 4096, 0, ok, ok, ok, 1 << 40, None) == L.FFT_EUNSUPPORTED
+    assert f(4096, 4096, 0, ok + 4, ok, ok, 1 << 40, None) == L.FFT_EALIGN
+    assert f(4096, 4096, 0, 1 << 30, ok, ok, (1 << 30) + 4096, None) == L.FFT_EINVAL
+    # the largest intermediates the array holds are 128 MiB; one beyond is refused
+    assert f(8192, 4096, 0, 1 << 30, ok, ok, 1 << 40, None) == L.FFT_EUNSUPPORTED
+    assert f(8192, 8192, 1, 1 << 30, ok, ok, 1 << 40, None) == L.FFT_EUNSUPPORTED
+    assert f(16384, 16384, 0, 1 << 30, ok, ok, 1 << 40, None) == L.FFT_EUNSUPPORTED
 
 
 def test_sar_workspace_bytes(L):
