@@ -185,6 +185,93 @@ def cross_lane_experiment(torch, api, flush, samples):
     return res
 
 
+def _with_env(env, fn):
+    """fn() with the kernel-shape variables set (read by plan creation and by
+    the SAR entry points on each call), restored afterwards."""
+    def run():
+        old = {k: os.environ.get(k) for k in env}
+        os.environ.update(env)
+        try:
+            return fn()
+        finally:
+            for k, v in old.items():
+                if v is None:
+                    os.environ.pop(k, None)
+                else:
+                    os.environ[k] = v
+    return run
+
+
+def twiddle_experiment(torch, api, flush, samples):
+    """The inter-stage twiddles formed by products of per-digit table reads
+    (the default) against every factor read from per-stage tables in lane
+    order, on the benchmark's FFT workloads and on the two SAR chains, each
+    kernel shape forced by its index in the size's lists.  Flushed samples are
+    interleaved across all cases after a clock warm-up."""
+    import workloads
+
+    res = {"experiment": "twiddles", "results": []}
+    cases = []
+    keep = []
+    for name, pairs in (("fft_n4096_b32768_fp32", ((0, "products"), (6, "stage tables"))),
+                        ("fft_n8192_b16384_fp32", ((0, "products"), (6, "stage tables"))),
+                        ("fft_n16384_b8192_fp32", ((4, "products"), (5, "stage tables"))),
+                        ("fft_n16384_b16384_fp16", ((4, "products"), (5, "stage tables")))):
+        w = workloads.FFT_WORKLOADS[name]
+        n, batch, st = w["n"], w["batch"], 0 if w["storage"] == "fp32" else 1
+        x = torch.from_numpy(workloads.fft_workload(name)).cuda()
+        out = torch.empty_like(x)
+        keep += [x, out]
+        for v, what in pairs:
+            plan = _with_env({"MI355FFT_ROW_VARIANT": str(v)}, lambda: api.Plan(n, batch, 1, n, st, -1))()
+            keep.append(plan)
+            cases.append({"name": f"{name} v{v}", "fn": (lambda p=plan, x=x, out=out: p.execute(x, out)),
+                          "bytes": 2 * n * batch * (8 if st == 0 else 4), "what": what, "workload": name})
+    sc = workloads.sar_scene()
+    raw = torch.from_numpy(sc.raw).cuda()
+    hr = torch.from_numpy(sc.range_ref).cuda()
+    ha = torch.from_numpy(sc.az_ref).cuda()
+    img = torch.empty_like(raw)
+    keep += [raw, hr, ha, img]
+    for inter in (0, 1):
+        ws = torch.empty(api._lib.sar_workspace_bytes(4096, 4096, inter), dtype=torch.uint8, device="cuda")
+        keep.append(ws)
+        for vr, vc, what in ((1, 3, "products in both passes"), (7, 3, "stage tables in the range pass"),
+                             (1, 4, "stage tables in the azimuth pass"), (7, 4, "stage tables in both passes")):
+            env = {"MI355FFT_ROW_VARIANT": str(vr), "MI355FFT_COL_VARIANT": str(vc)}
+            fn = _with_env(env, lambda inter=inter, ws=ws: api.sar_form_image(raw, hr, ha, inter, out=img, workspace=ws))
+            cases.append({"name": f"sar inter={inter} row v{vr} col v{vc}", "fn": fn,
+                          "bytes": (32 if inter == 0 else 24) * 4096 * 4096, "what": what,
+                          "workload": f"sar_4096x4096_{'fp32' if inter == 0 else 'fp16'}_inter"})
+    rd = workloads.rd_scene()
+    rraw = torch.from_numpy(rd.raw).cuda()
+    rhr = torch.from_numpy(rd.range_ref).cuda()
+    rout = torch.empty_like(rraw)
+    keep += [rraw, rhr, rout]
+    for inter in (0, 1):
+        ws = torch.empty(api._lib.sar_rd_workspace_bytes(4096, 4096, inter), dtype=torch.uint8, device="cuda")
+        keep.append(ws)
+        for vr, vc, vm, what in ((1, 3, 0, "products in every pass"), (7, 4, 2, "stage tables in every pass"),
+                                 (1, 3, 2, "stage tables in the migration pass")):
+            env = {"MI355FFT_ROW_VARIANT": str(vr), "MI355FFT_COL_VARIANT": str(vc), "MI355FFT_RCMC_VARIANT": str(vm)}
+            fn = _with_env(env, lambda inter=inter, ws=ws: api.sar_rd_form_image(rraw, rhr, rd.geometry, inter,
+                                                                                  out=rout, workspace=ws))
+            cases.append({"name": f"rd inter={inter} row v{vr} col v{vc} rcmc v{vm}", "fn": fn,
+                          "bytes": (48 if inter == 0 else 32) * 4096 * 4096, "what": what,
+                          "workload": f"rd_4096x4096_{'fp32' if inter == 0 else 'fp16'}_inter"})
+    ms = time_interleaved(torch, cases, flush, samples)
+    for c in cases:
+        med = float(np.median(ms[c["name"]]))
+        res["results"].append({"case": c["name"], "workload": c["workload"], "twiddles": c["what"],
+                               "flushed_ms": round(med, 5), "GB/s": round(c["bytes"] / (med * 1e-3) / 1e9, 1)})
+    for k in keep:
+        if hasattr(k, "close"):
+            k.close()
+    del keep, cases
+    torch.cuda.empty_cache()
+    return res
+
+
 def long_case(torch, api, n, batch):
     """A transform longer than the chip holds: the two-pass four-step form.
     GB/s counts the method's own 16 bytes per point (one read, one write);
@@ -645,7 +732,7 @@ def main():
     ap.add_argument("--ceilings", action="store_true",
                     help="instead of the benchmark: the memory-system ceilings (copy/read/write against working "
                          "set, the FFT kernels' block and strip patterns), one JSON line")
-    ap.add_argument("--experiment", choices=["matrix-units", "cross-lane"], default=None,
+    ap.add_argument("--experiment", choices=["matrix-units", "cross-lane", "twiddles"], default=None,
                     help="instead of the benchmark: FP16-storage N = 4096 / 16384 with the vector kernels, the "
                          "FP16 exchange and the matrix-core butterflies (one JSON line)")
     args = ap.parse_args()
@@ -662,6 +749,9 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.ceilings:
         print(json.dumps(ceilings(torch, Flusher(torch))), flush=True)
+        return
+    if args.experiment == "twiddles":
+        print(json.dumps(twiddle_experiment(torch, api, Flusher(torch), args.samples)), flush=True)
         return
     if args.experiment == "cross-lane":
         print(json.dumps(cross_lane_experiment(torch, api, Flusher(torch), args.samples)), flush=True)

@@ -115,15 +115,20 @@ struct Configs<4096> {
                        KCfg<4096, 16, 1, false, XCHG_FULL, 1, true, Radices<16, 16, 16>>,
                        KCfg<4096, 16, 1, false, XCHG_SPLIT, 1, true, Radices<16, 16, 16>>,
                        KCfg<4096, 16, 1, false, XCHG_FULL, 0, false, Radices<16, 16, 16>>,
-                       KCfg<4096, 16, 1, false, XCHG_SPLIT, 0, false, Radices<16, 16, 16>>>;
+                       KCfg<4096, 16, 1, false, XCHG_SPLIT, 0, false, Radices<16, 16, 16>>,
+                       // every factor from the per-stage tables
+                       KCfg<4096, 16, 1, false, XCHG_FULL, 2, false, Radices<16, 16, 16>, false>,
+                       KCfg<4096, 16, 1, false, XCHG_SPLIT, 2, false, Radices<16, 16, 16>>>;
     using Cols = KList<KCfg<4096, 32, 4, true, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>,
                        KCfg<4096, 32, 4, true, XCHG_SPLIT, 0, false, Radices<16, 16, 16>>,
                        KCfg<4096, 16, 4, true, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>,
-                       KCfg<4096, 32, 8, true, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>>;
+                       KCfg<4096, 32, 8, true, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>,
+                       KCfg<4096, 32, 8, true, XCHG_SPLIT, 2, false, Radices<16, 16, 16>>>;
     // 8-column strips measured fastest for both column passes: 64-byte row
     // pieces against 32 (plain 82 vs 117 us, matched 88 vs 100 us per 4096^2)
     using Rcmc = KList<KCfg<4096, 32, 8, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>,
-                       KCfg<4096, 16, 4, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>>;
+                       KCfg<4096, 16, 4, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>,
+                       KCfg<4096, 32, 8, false, XCHG_SPLIT, 2, false, Radices<16, 16, 16>>>;
     using RowsHalf = KList<KCfg<4096, 16, 1, false, XCHG_HALF, 1, false, Radices<16, 16, 16>>>;
     static constexpr int kRowDefault[2] = {0, 1}, kColDefault[2] = {3, 3};
     static constexpr int kRowMatched = 1, kColMatched = 3;
@@ -134,7 +139,9 @@ struct Configs<8192> {
                        KCfg<8192, 32, 1, false, XCHG_FULL, 1, false, Radices<32, 16, 16>>,
                        KCfg<8192, 16, 1, false, XCHG_SPLIT, 1, true, Radices<16, 16, 16, 2>>,
                        KCfg<8192, 16, 1, false, XCHG_FULL, 0, false, Radices<16, 16, 16, 2>>,
-                       KCfg<8192, 32, 1, false, XCHG_SPLIT, 1, false, Radices<32, 16, 16>>>;
+                       KCfg<8192, 32, 1, false, XCHG_SPLIT, 1, false, Radices<32, 16, 16>>,
+                       KCfg<8192, 32, 1, false, XCHG_SPLIT, 2, false, Radices<32, 16, 16>>,
+                       KCfg<8192, 16, 1, false, XCHG_SPLIT, 2, false, Radices<16, 16, 16, 2>>>;
     using Cols = KList<KCfg<8192, 32, 2, true, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 2>>,
                        KCfg<8192, 32, 2, true, XCHG_SPLIT, 0, false, Radices<16, 16, 16, 2>>>;
     using Rcmc = KList<KCfg<8192, 32, 4, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 2>>,
@@ -152,7 +159,8 @@ struct Configs<16384> {
                        KCfg<16384, 32, 1, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 4>>,
                        KCfg<16384, 32, 1, false, XCHG_SPLIT, 1, true, Radices<16, 16, 16, 4>>,
                        KCfg<16384, 32, 1, false, XCHG_SPLIT, 0, false, Radices<16, 16, 16, 4>>,
-                       KCfg<16384, 32, 1, false, XCHG_SPLIT, 1, false, Radices<32, 16, 32>>>;
+                       KCfg<16384, 32, 1, false, XCHG_SPLIT, 1, false, Radices<32, 16, 32>>,
+                       KCfg<16384, 32, 1, false, XCHG_SPLIT, 2, false, Radices<32, 16, 32>>>;
     using Cols = KList<KCfg<16384, 32, 1, true, XCHG_SPLIT, 0, false, Radices<16, 16, 16, 4>>,
                        KCfg<16384, 32, 1, true, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 4>>>;
     // three stages (32 x 16 x 32) against four: one exchange and one twiddle

@@ -29,7 +29,10 @@
 //          instructions (fft_lane.hpp).
 //   TWMODE 0: every inter-stage twiddle read from the table;
 //          1: one table read per base-4 digit of the radix, the rest formed
-//          by complex products (fewer loads, a few more FP32 operations).
+//          by complex products (fewer loads, a few more FP32 operations);
+//          2: every factor read from the stage's own table, laid out so that
+//          consecutive lanes read consecutive entries (no products: fewer
+//          FP32 operations than 1, more loads, each one coalesced).
 //   PERSIST the workgroup loops over its share of the batch and loads the
 //          next transform into a second register array while it computes the
 //          current one (the second-array idea of Section VI, used here to
@@ -148,7 +151,12 @@ constexpr int pow4(int i) { return i == 0 ? 1 : 4 * pow4(i - 1); }
 template <class K, int NS, int R>
 struct TwRegs {
     static constexpr int B = K::P / R;
-    static constexpr int LOADS = NS == 1 ? 0 : (K::TWMODE == 0 ? R - 1 : num_digits4(R));
+    // With the per-stage tables, the R - 1 factors of every butterfly would
+    // all be live across the exchange: 60 VGPRs at radix 16 with two
+    // butterflies per thread, 62 at radix 32, either of which spills.  Those
+    // stages read each butterfly's factors just before applying them instead.
+    static constexpr bool LATE = K::TWMODE == 2 && (B > 1 || R >= 32);
+    static constexpr int LOADS = NS == 1 || LATE ? 0 : (K::TWMODE == 1 ? num_digits4(R) : R - 1);
     float2 w[B][LOADS > 0 ? LOADS : 1];
 };
 
@@ -164,6 +172,14 @@ __device__ __forceinline__ void tw_issue(TwRegs<K, NS, R> &tr, int t, const floa
                 static_for<1, R>([&](auto rc) {
                     constexpr int r = decltype(rc)::value;
                     tr.w[q][r - 1] = tw[k * (r * STR)];
+                });
+            } else if constexpr (K::TWMODE == 2) {
+                // this stage's own table: row r - 1 holds W_(NS R)^(k r) at
+                // column k, so consecutive lanes read consecutive entries
+                constexpr long long OFF = stage_table_offset(K::N, NS, R);
+                static_for<1, R>([&](auto rc) {
+                    constexpr int r = decltype(rc)::value;
+                    tr.w[q][r - 1] = tw[OFF + (r - 1) * NS + k];
                 });
             } else {
                 static_for<0, TwRegs<K, NS, R>::LOADS>([&](auto ic) {
@@ -186,7 +202,7 @@ __device__ __forceinline__ void tw_issue(TwRegs<K, NS, R> &tr, int t, const floa
 template <class K, int NS, int R, int q, bool INV>
 __device__ __forceinline__ void tw_apply(const TwRegs<K, NS, R> &tr, float2 (&u)[R]) {
     auto mul = [](float2 a, float2 w) { return INV ? cmulc(a, w) : cmul(a, w); };
-    if constexpr (K::TWMODE == 0) {
+    if constexpr (K::TWMODE != 1) {
         static_for<1, R>([&](auto rc) { u[rc] = mul(u[rc], tr.w[q][rc - 1]); });
     } else {
         constexpr int D = TwRegs<K, NS, R>::LOADS;
@@ -313,7 +329,18 @@ __device__ __forceinline__ void run_stages(float2 (&v)[K::P], int t, int c, cons
         constexpr int q = decltype(qc)::value;
         float2 u[R];
         static_for<0, R>([&](auto rc) { u[rc] = v[q + rc * B]; });
-        if constexpr (NS > 1) tw_apply<K, NS, R, q, INV>(cur, u);
+        if constexpr (NS > 1 && TwRegs<K, NS, R>::LATE) {
+            // this butterfly's factors from the stage table, read now
+            constexpr long long OFF = stage_table_offset(K::N, NS, R);
+            const int k = (t + q * K::T) & (NS - 1);
+            static_for<1, R>([&](auto rc) {
+                constexpr int r = decltype(rc)::value;
+                const float2 w = tw[OFF + (r - 1) * NS + k];
+                u[r] = INV ? cmulc(u[r], w) : cmul(u[r], w);
+            });
+        } else if constexpr (NS > 1) {
+            tw_apply<K, NS, R, q, INV>(cur, u);
+        }
         Dft<R, INV>::run(u);
         static_for<0, R>([&](auto rc) { v[q + rc * B] = u[rc]; });
     });

@@ -87,6 +87,30 @@ __host__ __device__ constexpr RdTablesLayout rd_tables_layout(long long n_az, lo
                               round_up_256((long long)(kRcmcSub + 1) * kRcmcTaps * 8)};
 }
 
+// Twiddle tables.  The table of a length n holds W_n^m = exp(-2 pi i m / n)
+// for m < n, followed by per-stage tables: for every radix R in
+// {2, 4, 8, 16, 32} and every sub-transform length NS = 2, 4, ..., n / R, the
+// factors a stage of radix R on sub-transforms of length NS applies,
+// W_(NS R)^(k r), stored at [(r - 1) NS + k] for k < NS and 1 <= r < R.  A
+// butterfly of that stage then reads its R - 1 factors from R - 1 rows of one
+// stage table, and consecutive lanes (consecutive k) read consecutive entries.
+constexpr int kStageRadices[5] = {2, 4, 8, 16, 32};
+__host__ __device__ constexpr long long stage_table_entries(long long n, int r) {
+    return n / r >= 2 ? (long long)(r - 1) * (2 * (n / r) - 2) : 0;
+}
+// Offset (in entries, from the start of the length-n table) of the stage table
+// of radix r and sub-transform length ns (2 <= ns <= n / r).
+__host__ __device__ constexpr long long stage_table_offset(long long n, int ns, int r) {
+    long long off = n;
+    for (int i = 0; i < 5 && kStageRadices[i] < r; ++i) off += stage_table_entries(n, kStageRadices[i]);
+    return off + (long long)(r - 1) * (ns - 2);
+}
+__host__ __device__ constexpr long long twiddle_entries(long long n) {
+    long long e = n;
+    for (int i = 0; i < 5; ++i) e += stage_table_entries(n, kStageRadices[i]);
+    return e;
+}
+
 // The allocation-free SAR entry point keeps its tables and workspace in one
 // fixed device array per device (noalloc.hip), of kNoallocScratchBytes:
 // room for the twiddle tables, both reference spectra and an intermediate
@@ -94,7 +118,7 @@ __host__ __device__ constexpr RdTablesLayout rd_tables_layout(long long n_az, lo
 // intermediates).  noalloc_scratch returns the current device's copy of it;
 // the address is looked up once per device and kept.
 constexpr size_t kNoallocMaxImageBytes = size_t(128) << 20;
-constexpr size_t kNoallocScratchBytes = kNoallocMaxImageBytes + (size_t(1) << 20);
+constexpr size_t kNoallocScratchBytes = kNoallocMaxImageBytes + (size_t(3) << 20);
 hipError_t noalloc_scratch(int device, void **ptr);
 
 // Fills the range-Doppler tables (double-precision arithmetic on the device,

@@ -78,11 +78,23 @@ std::mutex g_tw_mutex;
 std::map<std::pair<int, int64_t>, float2 *> g_tw;
 
 void host_twiddles(int64_t n, std::vector<float2> &host) {
-    host.resize((size_t)n);
+    host.resize((size_t)mi355fft::twiddle_entries(n));
     const double two_pi = 6.283185307179586476925286766559;
     for (int64_t m = 0; m < n; ++m) {
         const double ang = two_pi * ((double)m / (double)n);
         host[(size_t)m] = make_float2((float)std::cos(ang), (float)-std::sin(ang));
+    }
+    // per-stage tables: W_(ns r)^(k j) at [(j - 1) ns + k], the angle reduced
+    // exactly (k j mod ns r) before it is scaled
+    for (int r : mi355fft::kStageRadices) {
+        for (int64_t ns = 2; ns <= n / r; ns *= 2) {
+            const int64_t base = mi355fft::stage_table_offset(n, (int)ns, r), len = ns * r;
+            for (int j = 1; j < r; ++j)
+                for (int64_t k = 0; k < ns; ++k) {
+                    const double ang = two_pi * ((double)((k * j) % len) / (double)len);
+                    host[(size_t)(base + (j - 1) * ns + k)] = make_float2((float)std::cos(ang), (float)-std::sin(ang));
+                }
+        }
     }
 }
 
@@ -97,9 +109,9 @@ int get_twiddles(int device, int64_t n, const float2 **out) {
     std::vector<float2> host;
     host_twiddles(n, host);
     float2 *dev = nullptr;
-    hipError_t e = hipMalloc((void **)&dev, sizeof(float2) * (size_t)n);
+    hipError_t e = hipMalloc((void **)&dev, sizeof(float2) * host.size());
     if (e != hipSuccess) return map_hip(e);
-    e = hipMemcpy(dev, host.data(), sizeof(float2) * (size_t)n, hipMemcpyHostToDevice);
+    e = hipMemcpy(dev, host.data(), sizeof(float2) * host.size(), hipMemcpyHostToDevice);
     if (e != hipSuccess) {
         (void)hipFree(dev);
         return map_hip(e);
@@ -788,7 +800,12 @@ int sar_run(int64_t n_az, int64_t n_rg, int inter_storage, const void *raw, cons
 // The allocation-free SAR entry point's fixed device array (noalloc.hip):
 // the twiddle tables of every length 64 ... 16384 and the two-level tables of
 // 8192 and 16384, filled once per device, then the chain's workspace.
-constexpr size_t kNaTwBytes = (size_t)(2 * 16384 - 64) * sizeof(float2);  // lengths 64 .. 16384
+constexpr size_t na_tw_entries_below(int64_t n) {  // tables of the lengths 64 .. n / 2
+    size_t e = 0;
+    for (int64_t m = 64; m < n; m *= 2) e += (size_t)mi355fft::twiddle_entries(m);
+    return e;
+}
+constexpr size_t kNaTwBytes = na_tw_entries_below(32768) * sizeof(float2);  // lengths 64 .. 16384
 constexpr size_t kNaFtabOffset = kNaTwBytes;
 constexpr size_t kNaFtabBytes = (size_t)(192 + 256) * sizeof(float2);  // 8192: 128 + 64; 16384: 128 + 128
 constexpr size_t kNaWorkspaceOffset = mi355fft::round_up_256(kNaFtabOffset + kNaFtabBytes);
@@ -796,7 +813,7 @@ static_assert(kNaWorkspaceOffset + 2 * 16384 * sizeof(float2) + mi355fft::kNoall
                   mi355fft::kNoallocScratchBytes,
               "the fixed array holds the tables, both spectra and the largest intermediate");
 
-size_t na_tw_offset(int64_t n) { return (size_t)(n - 64) * sizeof(float2); }  // 64 + 128 + ... + n/2 = n - 64
+size_t na_tw_offset(int64_t n) { return na_tw_entries_below(n) * sizeof(float2); }
 size_t na_ftab_offset(int64_t n) { return kNaFtabOffset + (n == 8192 ? 0 : 192 * sizeof(float2)); }
 
 std::mutex g_na_mutex;
