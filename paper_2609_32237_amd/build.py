@@ -25,7 +25,7 @@ COMMON = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I", INCLUDE, "-I", CSRC,
 ] + [f"-D{d}" for d in os.environ.get("MI355FFT_DEFINES", "").split() if d]
-SOURCES = ["fft_small.hip", "fft_n1024.hip", "fft_n2048.hip", "fft_n4096.hip", "fft_n8192.hip", "fft_n16384.hip", "rd_tables.hip",
+SOURCES = ["fft_small.hip", "fft_n1024.hip", "fft_n2048.hip", "fft_n4096.hip", "fft_n8192.hip", "fft_n16384.hip",
            "noalloc.hip", "runtime.cpp"]
 # the memory-ceiling kernels of the benchmark: a library of their own, which
 # the FFT library neither links nor calls

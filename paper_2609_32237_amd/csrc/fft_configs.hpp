@@ -217,7 +217,7 @@ hipError_t with_variant(int idx, KList<K, Ks...>, F &&f) {
 
 // Supported (layout, storage, direction, epilogue) combinations:
 //   plain FFT:  rows or columns, input storage == output storage, either direction;
-//   matched:    forward, multiply by conj(spec) * scale, inverse:
+//   matched:    forward, multiply by conj(spec) (spec carries 1/N), inverse:
 //               rows read FP32 and write FP32 or FP16 (range compression);
 //               columns read FP32 or FP16 and write FP32 (azimuth compression);
 //   scaled:     columns, forward, input storage == output storage (the azimuth

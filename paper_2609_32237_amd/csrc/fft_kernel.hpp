@@ -41,14 +41,16 @@
 // their latency hides behind the exchange.
 //
 // Optional fused epilogue (Section X, range compression in one kernel):
-// after the forward stages, X[k] <- X[k] * conj(H[k]) * scale, then the
-// inverse stages run on the same registers with no trip to memory.
+// after the forward stages, X[k] <- X[k] * conj(H[k]) (H carrying the
+// chain's 1/N), then the inverse stages run on the same registers with no
+// trip to memory.
 #pragma once
 
 #include <atomic>
 
 #include "fft_device.hpp"
 #include "fft_launch.h"
+#include "rd_tables.hpp"
 
 namespace mi355fft {
 
@@ -712,8 +714,10 @@ __device__ __forceinline__ void store_remapped(float2 (&v)[K::P], void *__restri
 
 // The whole on-chip computation of one transform (first exchange of the
 // kernel may skip its leading barrier).
+// t and c are the caller's lane coordinates; the fused inverse launders them
+// in place (below), so the caller keeps one copy of them, not two.
 template <class K, bool INV, int EPI, bool FIRST_X>
-__device__ __forceinline__ void transform(float2 (&v)[K::P], int t, int c, const float2 *__restrict__ tw,
+__device__ __forceinline__ void transform(float2 (&v)[K::P], int &t, int &c, const float2 *__restrict__ tw,
                                           const float2 *__restrict__ spec, float scale, float *lds,
                                           int spec_off = 0, int spec_shift = 0) {
     constexpr bool MF = EPI == EPI_MATCHED || EPI == EPI_MATCHED_Y;
@@ -724,18 +728,19 @@ __device__ __forceinline__ void transform(float2 (&v)[K::P], int t, int c, const
         run_fft<K, INV, FIRST_X>(typename K::Rad{}, v, t, c, tw, lds);
     }
     if constexpr (MF) {
-        // X[k] * conj(H[k]) * scale, k = t + T*i, then the inverse transform.
+        // X[k] * conj(H[k]), k = t + T*i, then the inverse transform.
         // The scheduling fences keep the two transforms' register lifetimes
         // apart (interleaving them costs occupancy); H is read eight values
         // at a time between fences, so it never needs a second register
         // array beside X.
         __builtin_amdgcn_sched_barrier(0);
+        // (the chains fold their power-of-two 1/N into the spectrum, which is
+        // exact, so no scale is applied here)
         constexpr int HC = K::P < 8 ? K::P : 8;
         static_for<0, K::P / HC>([&](auto jc) {
             static_for<0, HC>([&](auto ec) {
                 constexpr int i = decltype(jc)::value * HC + decltype(ec)::value;
-                const float2 y = cmulc(v[i], spec[spec_off + ((t + K::T * i) << spec_shift)]);
-                v[i] = make_float2(y.x * scale, y.y * scale);
+                v[i] = cmulc(v[i], spec[spec_off + ((t + K::T * i) << spec_shift)]);
             });
             __builtin_amdgcn_sched_barrier(0);
         });
@@ -745,10 +750,11 @@ __device__ __forceinline__ void transform(float2 (&v)[K::P], int t, int c, const
         // alive across the multiply to reuse them (over 100 more VGPRs on the
         // 8-column kernels, which then spill); passing the pointer and the
         // lane coordinates through an empty asm statement hides the equality.
+        // The coordinates are laundered in place, and the store that follows
+        // uses the laundered copies.
         const float2 *tw2 = tw;
-        int t2 = t, c2 = c;
-        asm volatile("" : "+s"(tw2), "+v"(t2), "+v"(c2));
-        run_fft<K, !INV, false>(typename K::Rad{}, v, t2, c2, tw2, lds);
+        asm volatile("" : "+s"(tw2), "+v"(t), "+v"(c));
+        run_fft<K, !INV, false>(typename K::Rad{}, v, t, c, tw2, lds);
     }
     if constexpr (EPI == EPI_SCALE) {
         static_for<0, K::P>([&](auto ic) {
@@ -800,8 +806,8 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
         out = reinterpret_cast<char *>(out) + out_off * Store<OUT_ST>::BYTES;
     }
     const int tid = threadIdx.x;
-    const int c = K::COLS ? (tid & (K::C - 1)) : (tid >> K::LOG_T);
-    const int t = K::COLS ? (tid >> K::LOG_C) : (tid & (K::T - 1));
+    int c = K::COLS ? (tid & (K::C - 1)) : (tid >> K::LOG_T);
+    int t = K::COLS ? (tid >> K::LOG_C) : (tid & (K::T - 1));
     float2 v[K::P];
     if constexpr (!K::PERSIST) {
         // strips per 128-byte line, from the narrower of the two sides' pieces;
@@ -815,6 +821,12 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
         constexpr int GROUP = EPI == EPI_RCMC && LINE_GROUP < 8 ? 8 : LINE_GROUP;
         const long long blk = logical_block<GROUP>(a.xcd_remap);
         const bool valid = blk * K::C + c < a.batch;
+        if constexpr (EPI == EPI_SCALE) {
+            // the range-Doppler chain's tables for the migration pass that follows
+            if (a.rd_tables)
+                rd_table_entry((long long)blockIdx.x * K::THREADS + threadIdx.x, K::N, a.batch, a.rd_geo,
+                               a.rd_interp, a.rd_tables);
+        }
         if constexpr (EPI == EPI_RCMC) {
             rcmc_load<K, IN_ST>(v, in, blk, c, t, valid, a, spec, lds);
             transform<K, INV, EPI_NONE, true>(v, t, c, tw, spec, a.scale, lds);

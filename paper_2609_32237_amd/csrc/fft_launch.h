@@ -37,8 +37,8 @@ hipError_t launch_kernel(void (*kern)(Params...), dim3 grid, dim3 block, hipStre
 enum { LAYOUT_ROWS = 0, LAYOUT_COLS = 1, LAYOUT_RCMC = 2, LAYOUT_ROWS_HALF = 3 };
 // Per-kernel fusions around the transform:
 //   EPI_NONE     the plain transform;
-//   EPI_MATCHED  forward, X * conj(spec) * scale, inverse (range or azimuth
-//                compression in one pass);
+//   EPI_MATCHED  forward, X * conj(spec), inverse (range or azimuth
+//                compression in one pass; spec carries the 1/N scale);
 //   EPI_SCALE    forward, output * scale (the azimuth FFT with its 1/N_a),
 //                column strips in, written as rows (out_stride 1);
 //   EPI_RCMC     the load stage gathers, interpolates and phase-rotates the
@@ -47,8 +47,8 @@ enum { LAYOUT_ROWS = 0, LAYOUT_COLS = 1, LAYOUT_RCMC = 2, LAYOUT_ROWS_HALF = 3 }
 //                is written as columns; `spec` points to the range-Doppler
 //                tables below.
 //   EPI_MATCHED_Y  the middle pass of a matched filter along long columns in
-//                four-step form: forward, X[k] * conj(spec[y + (k << spec_shift)])
-//                * scale, inverse, then output j times conj(W^(y j)) from tab2
+//                four-step form: forward, X[k] * conj(spec[y + (k << spec_shift)]),
+//                inverse, then output j times conj(W^(y j)) from tab2
 //                (y = blockIdx.y);
 //   EPI_TWIDDLE_Y  middle pass of a three-pass transform: plain column strips,
 //                output point k of problem blockIdx.y times W^(blockIdx.y k)
@@ -121,11 +121,12 @@ constexpr size_t kNoallocMaxImageBytes = size_t(128) << 20;
 constexpr size_t kNoallocScratchBytes = kNoallocMaxImageBytes + (size_t(3) << 20);
 hipError_t noalloc_scratch(int device, void **ptr);
 
-// Fills the range-Doppler tables (double-precision arithmetic on the device,
-// rounded once to FP32 or split into FP32 hi + lo pairs).
-hipError_t launch_rd_tables(long long n_az, long long n_rg, double wavelength, double speed, double prf,
-                            double range_bin, double r_near, const float2 *interp_src, void *tables,
-                            hipStream_t s);
+// Acquisition geometry the range-Doppler tables are computed from (metres,
+// Hz, m/s); the tables are filled by the azimuth-FFT pass (rd_tables.hpp) in
+// double precision and rounded once to FP32 or split into hi + lo pairs.
+struct RdGeometry {
+    double wavelength, speed, prf, range_bin, r_near;
+};
 
 struct KArgs {
     long long batch;       // transforms
@@ -152,6 +153,12 @@ struct KArgs {
     // the outer transform's factors
     int spec_shift;
     const float2 *tab2;
+    // EPI_SCALE: when rd_tables is set, thread g = blockIdx.x * THREADS +
+    // threadIdx.x first writes entry g of the range-Doppler tables (n_az = the
+    // transform length, n_rg = batch) from the geometry and interpolator rows
+    RdGeometry rd_geo;
+    const float2 *rd_interp;
+    void *rd_tables;
 };
 
 // Fills the addressing fields of `a` for workgroups of `c` transforms of `n`

@@ -700,8 +700,8 @@ int sar_long_azimuth(int64_t n_az, int64_t n_rg, const void *raw, void *out, voi
     using mi355fft::LAYOUT_COLS;
     const int64_t n1 = 128, n2 = n_az / n1;
     const int log2s = (ilog2(n_az) + 1) / 2;
-    // range pass into `out`
-    const KArgs ar{n_az, 1, n_rg, n_rg, (float)(1.0 / (double)n_rg), 0};
+    // range pass into `out` (H_r already carries 1/n_rg)
+    const KArgs ar{n_az, 1, n_rg, n_rg, 1.0f, 0};
     hipError_t e = launch_fft(n_rg, vrow, mi355fft::LAYOUT_ROWS, FFT_STORAGE_FP32, FFT_STORAGE_FP32, 0,
                               mi355fft::EPI_MATCHED, raw, out, t.tw_rg, h_rg, ar, stream);
     if (e != hipSuccess) return map_hip(e);
@@ -714,7 +714,7 @@ int sar_long_azimuth(int64_t n_az, int64_t n_rg, const void *raw, void *out, voi
     e = launch_fft(n1, -1, LAYOUT_COLS, FFT_STORAGE_FP32, FFT_STORAGE_FP32, 0, mi355fft::EPI_TWIDDLE_Y, out, mid,
                    t.tw1, t.ftab, b1, stream);
     if (e != hipSuccess) return map_hip(e);
-    KArgs b2{n_rg, n1 * n_rg, 1, 1, (float)(1.0 / (double)n_az), strip_map(n1 * n_rg * 8)};
+    KArgs b2{n_rg, n1 * n_rg, 1, 1, 1.0f, strip_map(n1 * n_rg * 8)};  // H_a carries 1/n_az
     b2.outer = (int)n1;
     b2.outer_in_dist = b2.outer_out_dist = n_rg;
     b2.aux = log2s;
@@ -763,19 +763,22 @@ int sar_run(int64_t n_az, int64_t n_rg, int inter_storage, const void *raw, cons
     using mi355fft::LAYOUT_ROWS;
     hipError_t e;
 
-    // reference spectra H = FFT(ref) into the workspace; the passes multiply by
-    // conj(H).  Equal lengths: one launch of two transforms (the input distance
-    // is the signed distance between the two reference buffers).
+    // reference spectra into the workspace, each with its pass's scale folded
+    // in (a power of two, so exact): H_r / n_rg and H_a / n_az; the passes
+    // multiply by their conjugates.  Equal lengths: one launch of two
+    // transforms (the input distance is the signed distance between the two
+    // reference buffers).
+    const float s_rg = (float)(1.0 / (double)n_rg), s_az = (float)(1.0 / (double)n_az);
     if (n_rg == n_az) {
         const long long gap = ((const char *)az_ref - (const char *)range_ref) / (long long)sizeof(float2);
-        const KArgs a{2, 1, gap, n_rg, 1.0f, 0};
+        const KArgs a{2, 1, gap, n_rg, s_rg, 0};
         e = launch_fft(n_rg, vrow, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, range_ref, h_rg, t.tw_rg, nullptr, a, stream);
         if (e != hipSuccess) return map_hip(e);
     } else {
-        const KArgs a1{1, 1, n_rg, n_rg, 1.0f, 0};
+        const KArgs a1{1, 1, n_rg, n_rg, s_rg, 0};
         e = launch_fft(n_rg, vrow, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, range_ref, h_rg, t.tw_rg, nullptr, a1, stream);
         if (e != hipSuccess) return map_hip(e);
-        const KArgs a2{1, 1, n_az, n_az, 1.0f, 0};
+        const KArgs a2{1, 1, n_az, n_az, s_az, 0};
         e = launch_fft(n_az, vref, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, az_ref, h_az, t.tw_az, nullptr, a2, stream);
         if (e != hipSuccess) return map_hip(e);
     }
@@ -784,14 +787,14 @@ int sar_run(int64_t n_az, int64_t n_rg, int inter_storage, const void *raw, cons
         return sar_long_azimuth(n_az, n_rg, raw, out, mid, h_rg, h_az, t, vrow, stream);
     }
 
-    // pass 1, rows (range): FFT, * conj(H_r) / n_rg, IFFT -> intermediate
-    const KArgs ar{n_az, 1, n_rg, n_rg, (float)(1.0 / (double)n_rg), 0};
+    // pass 1, rows (range): FFT, * conj(H_r / n_rg), IFFT -> intermediate
+    const KArgs ar{n_az, 1, n_rg, n_rg, 1.0f, 0};
     e = launch_fft(n_rg, vrow, LAYOUT_ROWS, FFT_STORAGE_FP32, inter_storage, 0, EPI_MATCHED, raw, mid, t.tw_rg, h_rg,
                    ar, stream);
     if (e != hipSuccess) return map_hip(e);
 
-    // pass 2, columns (azimuth): FFT, / n_az * conj(H_a), IFFT -> image
-    const KArgs ac{n_rg, n_rg, 1, 1, (float)(1.0 / (double)n_az), strip_map(n_rg * 8)};
+    // pass 2, columns (azimuth): FFT, * conj(H_a / n_az), IFFT -> image
+    const KArgs ac{n_rg, n_rg, 1, 1, 1.0f, strip_map(n_rg * 8)};
     e = launch_fft(n_az, vcol, LAYOUT_COLS, inter_storage, FFT_STORAGE_FP32, 0, EPI_MATCHED, mid, out, t.tw_az, h_az,
                    ac, stream);
     return map_hip(e);
@@ -957,15 +960,13 @@ int sar_rd_form_image(int64_t n_az, int64_t n_rg, int inter_storage, const sar_g
     void *tables = wsb + rd_tables_offset(n_rg);
     void *zt = wsb + rd_mid_offset(n_az, n_rg);
 
-    e = launch_rd_tables(n_az, n_rg, g[0], g[1], g[2], g[3], g[4], interp, tables, stream);
-    if (e != hipSuccess) return map_hip(e);
-    const KArgs aref{1, 1, n_rg, n_rg, 1.0f, 0};
+    const KArgs aref{1, 1, n_rg, n_rg, (float)(1.0 / (double)n_rg), 0};  // H_r / n_rg (exact)
     e = launch_fft(n_rg, vrow, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, range_ref, h_rg, tw_rg, nullptr, aref, stream);
     if (e != hipSuccess) return map_hip(e);
     // 1: range compression, rows: FFT, * conj(H_r) / n_rg, IFFT.  The
     //    range-compressed image is kept in `out`, which the last pass
-    //    overwrites with the focused image.
-    const KArgs ar{n_az, 1, n_rg, n_rg, (float)(1.0 / (double)n_rg), 0};
+    //    overwrites with the focused image.  H_r carries the 1/n_rg.
+    const KArgs ar{n_az, 1, n_rg, n_rg, 1.0f, 0};
     e = launch_fft(n_rg, vrow, LAYOUT_ROWS, FFT_STORAGE_FP32, inter_storage, 0, EPI_MATCHED, raw, out, tw_rg, h_rg,
                    ar, stream);
     if (e != hipSuccess) return map_hip(e);
@@ -973,6 +974,11 @@ int sar_rd_form_image(int64_t n_az, int64_t n_rg, int inter_storage, const sar_g
     //    per range bin (the transposed range-Doppler image)
     KArgs ab{n_rg, n_rg, 1, n_az, (float)(1.0 / (double)n_az), strip_map(n_rg * 8)};
     ab.out_stride = 1;
+    //    this pass also fills the tables of the migration pass (one entry per
+    //    thread: its n_rg * n_az / P threads cover n_az, n_rg and the rows)
+    ab.rd_geo = RdGeometry{g[0], g[1], g[2], g[3], g[4]};
+    ab.rd_interp = interp;
+    ab.rd_tables = tables;
     e = launch_fft(n_az, vcol, LAYOUT_COLS, inter_storage, inter_storage, 0, EPI_SCALE, out, zt, tw_az, nullptr, ab,
                    stream);
     if (e != hipSuccess) return map_hip(e);
