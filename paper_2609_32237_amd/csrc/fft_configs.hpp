@@ -123,15 +123,24 @@ struct Configs<4096> {
                        KCfg<4096, 32, 4, true, XCHG_SPLIT, 0, false, Radices<16, 16, 16>>,
                        KCfg<4096, 16, 4, true, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>,
                        KCfg<4096, 32, 8, true, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>,
-                       KCfg<4096, 32, 8, true, XCHG_SPLIT, 2, false, Radices<16, 16, 16>>>;
+                       KCfg<4096, 32, 8, true, XCHG_SPLIT, 2, false, Radices<16, 16, 16>>,
+                       // two radix-64 stages, 64 points per thread: one exchange per
+                       // transform instead of two, and fewer VALU instructions per
+                       // point (100 against 106 for the matched pass)
+                       KCfg<4096, 64, 8, true, XCHG_SPLIT, 1, false, Radices<64, 64>>,
+                       KCfg<4096, 64, 4, true, XCHG_SPLIT, 1, false, Radices<64, 64>>>;
     // 8-column strips measured fastest for both column passes: 64-byte row
-    // pieces against 32 (plain 82 vs 117 us, matched 88 vs 100 us per 4096^2)
+    // pieces against 32 (plain 82 vs 117 us, matched 88 vs 100 us per 4096^2
+    // with 32 points per thread).  Radix 64, 8 columns, 30 interleaved
+    // flushed samples per 4096^2 workload: plain 75.2 against 78.8 us (FP32)
+    // and 53.8 against 55.0 (FP16); SAR chain 143.1 against 157.1 us (FP32
+    // intermediate) and 131.3 against 135.7 (FP16).
     using Rcmc = KList<KCfg<4096, 32, 8, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>,
                        KCfg<4096, 16, 4, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>,
                        KCfg<4096, 32, 8, false, XCHG_SPLIT, 2, false, Radices<16, 16, 16>>>;
     using RowsHalf = KList<KCfg<4096, 16, 1, false, XCHG_HALF, 1, false, Radices<16, 16, 16>>>;
-    static constexpr int kRowDefault[2] = {0, 1}, kColDefault[2] = {3, 3};
-    static constexpr int kRowMatched = 1, kColMatched = 3;
+    static constexpr int kRowDefault[2] = {0, 1}, kColDefault[2] = {5, 5};
+    static constexpr int kRowMatched = 1, kColMatched = 5;
 };
 template <>
 struct Configs<8192> {
@@ -197,6 +206,45 @@ struct SmallRows<2048> {
     static constexpr long long below = 2 * 256;
 };
 
+template <int I, class L>
+struct KAt;
+template <class K, class... Ks>
+struct KAt<0, KList<K, Ks...>> {
+    using type = K;
+};
+template <int I, class K, class... Ks>
+struct KAt<I, KList<K, Ks...>> {
+    using type = typename KAt<I - 1, KList<Ks...>>::type;
+};
+
+// Column shapes for the four-step epilogues (EPI_TWIDDLE, EPI_TWIDDLE_Y,
+// EPI_MATCHED_Y), which hold at most 32 points per thread: the size's default
+// shapes unless a size names others.
+template <int N>
+struct FourStepCols {
+    static constexpr int plain[2] = {Configs<N>::kColDefault[0], Configs<N>::kColDefault[1]};
+    static constexpr int matched = Configs<N>::kColMatched;
+};
+template <>
+struct FourStepCols<4096> {
+    static constexpr int plain[2] = {3, 3};
+    static constexpr int matched = 3;
+};
+
+// The column shape of the scaled transform (EPI_SCALE, the range-Doppler
+// chain's azimuth pass).  At 4096 points the 4-column radix-64 strips
+// measured 205.7 against 214.3 us (8 columns) per range-Doppler chain with
+// FP32 intermediates, 190.7 against 191.9 with FP16 (30 interleaved flushed
+// samples each), although 8 columns are faster for the plain transform.
+template <int N>
+struct ScaleCols {
+    static constexpr int v[2] = {Configs<N>::kColDefault[0], Configs<N>::kColDefault[1]};
+};
+template <>
+struct ScaleCols<4096> {
+    static constexpr int v[2] = {6, 6};
+};
+
 template <class L>
 struct KListSize;
 template <class... Ks>
@@ -250,7 +298,7 @@ hipError_t dispatch_cfg_full(int in_st, int out_st, int inv, int epi, const void
         }
     }
     if (epi == EPI_TWIDDLE) {
-        if constexpr (K::COLS && !K::PERSIST) {
+        if constexpr (K::COLS && !K::PERSIST && K::P <= 32) {
             if (in_st != out_st) return hipErrorInvalidValue;
             if (in_st == 0)
                 return inv ? launch_one<K, 0, 0, true, EPI_TWIDDLE>(in, out, tw, spec, a, s)
@@ -262,7 +310,7 @@ hipError_t dispatch_cfg_full(int in_st, int out_st, int inv, int epi, const void
         }
     }
     if (epi == EPI_TWIDDLE_Y) {
-        if constexpr (K::COLS && !K::PERSIST) {
+        if constexpr (K::COLS && !K::PERSIST && K::P <= 32) {
             if (in_st != out_st) return hipErrorInvalidValue;
             if (in_st == 0)
                 return inv ? launch_one<K, 0, 0, true, EPI_TWIDDLE_Y>(in, out, tw, spec, a, s)
@@ -274,7 +322,7 @@ hipError_t dispatch_cfg_full(int in_st, int out_st, int inv, int epi, const void
         }
     }
     if (epi == EPI_MATCHED_Y) {
-        if constexpr (K::COLS && !K::PERSIST) {
+        if constexpr (K::COLS && !K::PERSIST && K::P <= 32) {
             if (inv || in_st != 0 || out_st != 0) return hipErrorInvalidValue;
             return launch_one<K, 0, 0, false, EPI_MATCHED_Y>(in, out, tw, spec, a, s);
         } else {
@@ -350,8 +398,23 @@ hipError_t dispatch(int variant, int layout, int in_st, int out_st, int inv, int
         if (variant < 0 && !mf && epi == EPI_NONE && a.batch < SmallRows<N>::below) v = SmallRows<N>::variant;
         return with_variant(v, typename Configs<N>::Rows{}, f);
     }
-    const int v = variant >= 0 ? variant : mf ? Configs<N>::kColMatched : Configs<N>::kColDefault[half];
-    return with_variant(v, typename Configs<N>::Cols{}, f);
+    using Cols = typename Configs<N>::Cols;
+    static_assert(KAt<FourStepCols<N>::plain[0], Cols>::type::P <= 32 &&
+                      KAt<FourStepCols<N>::plain[1], Cols>::type::P <= 32 &&
+                      KAt<FourStepCols<N>::matched, Cols>::type::P <= 32,
+                  "the four-step epilogues hold at most 32 points per thread");
+    const bool four_step = epi == EPI_TWIDDLE || epi == EPI_TWIDDLE_Y || epi == EPI_MATCHED_Y;
+    int v = variant;
+    if (v < 0) {
+        if (four_step) {
+            v = mf ? FourStepCols<N>::matched : FourStepCols<N>::plain[half];
+        } else if (epi == EPI_SCALE) {
+            v = ScaleCols<N>::v[half];
+        } else {
+            v = mf ? Configs<N>::kColMatched : Configs<N>::kColDefault[half];
+        }
+    }
+    return with_variant(v, Cols{}, f);
 }
 
 template <int N>
