@@ -150,7 +150,9 @@ struct Configs<8192> {
                        KCfg<8192, 16, 1, false, XCHG_FULL, 0, false, Radices<16, 16, 16, 2>>,
                        KCfg<8192, 32, 1, false, XCHG_SPLIT, 1, false, Radices<32, 16, 16>>,
                        KCfg<8192, 32, 1, false, XCHG_SPLIT, 2, false, Radices<32, 16, 16>>,
-                       KCfg<8192, 16, 1, false, XCHG_SPLIT, 2, false, Radices<16, 16, 16, 2>>>;
+                       KCfg<8192, 16, 1, false, XCHG_SPLIT, 2, false, Radices<16, 16, 16, 2>>,
+                       // the second stage's 240 factors from LDS (twiddle mode 3)
+                       KCfg<8192, 16, 1, false, XCHG_SPLIT, 3, false, Radices<16, 16, 16, 2>>>;
     using Cols = KList<KCfg<8192, 32, 2, true, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 2>>,
                        KCfg<8192, 32, 2, true, XCHG_SPLIT, 0, false, Radices<16, 16, 16, 2>>>;
     using Rcmc = KList<KCfg<8192, 32, 4, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 2>>,
@@ -158,8 +160,10 @@ struct Configs<8192> {
     // binary16 exchange: three stages 5.5 TB/s, four stages 4.8
     using RowsHalf = KList<KCfg<8192, 32, 1, false, XCHG_HALF, 1, false, Radices<32, 16, 16>>,
                            KCfg<8192, 16, 1, false, XCHG_HALF, 1, false, Radices<16, 16, 16, 2>>>;
-    // FP16: 32 points per thread in three stages, 5.7 vs 4.9 TB/s
-    static constexpr int kRowDefault[2] = {0, 4}, kColDefault[2] = {0, 0};
+    // FP16: 32 points per thread in three stages, 5.7 vs 4.9 TB/s.  FP32:
+    // the second stage's factors from LDS, 5,740 against 5,607 GB/s flushed
+    // and 5,700-5,731 against 5,318-5,604 back to back (same box, one run)
+    static constexpr int kRowDefault[2] = {7, 4}, kColDefault[2] = {0, 0};
     static constexpr int kRowMatched = 0, kColMatched = 0;
 };
 template <>

@@ -32,7 +32,10 @@
 //          by complex products (fewer loads, a few more FP32 operations);
 //          2: every factor read from the stage's own table, laid out so that
 //          consecutive lanes read consecutive entries (no products: fewer
-//          FP32 operations than 1, more loads, each one coalesced).
+//          FP32 operations than 1, more loads, each one coalesced);
+//          3: stages whose own table is small (at most kLdsTwEntries
+//          factors) read every factor from a copy of that table in LDS, which
+//          the workgroup fills once; the other stages work as in mode 1.
 //   PERSIST the workgroup loops over its share of the batch and loads the
 //          next transform into a second register array while it computes the
 //          current one (the second-array idea of Section VI, used here to
@@ -71,6 +74,26 @@ struct RadProd<Radices<R, Rs...>> {
     static constexpr int value = R * RadProd<Radices<Rs...>>::value;
 };
 
+// Twiddle mode 3: a stage (NS, R) with NS > 1 takes its factors from LDS
+// when its table, (R - 1) * NS factors, has at most kLdsTwEntries of them
+// (stage tables exist for radices up to 32).
+constexpr int kLdsTwEntries = 1024;
+constexpr bool lds_tw_stage(int ns, int r) { return ns > 1 && r <= 32 && (r - 1) * ns <= kLdsTwEntries; }
+
+// Offset (in factors) of stage ns's table in the workgroup's LDS copy, and
+// (ns = 0) the total size of the copy, for the radix schedule Rs.
+template <int... Rs>
+constexpr int lds_tw_offset(Radices<Rs...>, int ns_target) {
+    constexpr int rs[] = {Rs...};
+    int ns = 1, off = 0;
+    for (int i = 0; i < (int)sizeof...(Rs); ++i) {
+        if (ns == ns_target) return off;
+        if (lds_tw_stage(ns, rs[i])) off += (rs[i] - 1) * ns;
+        ns *= rs[i];
+    }
+    return off;
+}
+
 template <int N_, int P_, int C_, bool COLS_, int XCHG_, int TWMODE_, bool PERSIST_, class Rad_, bool NTROW_ = true>
 struct KCfg {
     static constexpr int N = N_, P = P_, T = N_ / P_, C = C_, THREADS = T * C;
@@ -90,7 +113,12 @@ struct KCfg {
     static constexpr int ROW_SPAN = N_ + (N_ >> PADSH) + RSKEW;
     static constexpr int SPAN = COLS_ ? (N_ * C_ + ((N_ * C_) >> PADSH)) : C_ * ROW_SPAN;
     // the cross-lane kernels keep each transform inside one wave: no LDS
-    static constexpr int LDS_FLOATS = XCHG_ == XCHG_LANE ? 1 : XCHG_ == XCHG_FULL ? 2 * SPAN : SPAN;
+    static constexpr int XFLOATS = XCHG_ == XCHG_LANE ? 1 : XCHG_ == XCHG_FULL ? 2 * SPAN : SPAN;
+    // twiddle mode 3: the LDS copy of the small stage tables (float2 each),
+    // after the exchange area (8-byte aligned)
+    static constexpr int TWL_OFF = (XFLOATS + 1) & ~1;
+    static constexpr int TWL = TWMODE_ == 3 ? lds_tw_offset(Rad_{}, 0) : 0;
+    static constexpr int LDS_FLOATS = TWL > 0 ? TWL_OFF + 2 * TWL : XFLOATS;
     // Waves per SIMD the LDS allows (a CU has 4 SIMDs and 160 KiB of LDS),
     // capped at 4: asking the compiler for this occupancy keeps it from
     // spending registers the LDS limit would not let other waves use anyway,
@@ -105,6 +133,8 @@ struct KCfg {
     static_assert(LDS_FLOATS * 4 <= 160 * 1024, "gfx950 LDS is 160 KiB per workgroup");
     static_assert(XCHG_ != XCHG_LANE || (N_ == 1024 && P_ == 16 && !COLS_ && !PERSIST_),
                   "cross-lane exchanges: 1024-point rows, one transform per wave");
+    static_assert(TWMODE_ != 3 || (TWL > 0 && XCHG_ != XCHG_LANE && !PERSIST_),
+                  "twiddle mode 3: a small stage table, an LDS exchange, one transform per workgroup");
 };
 
 template <class... Ks>
@@ -150,15 +180,23 @@ constexpr int lds_offset(int delta) {
 constexpr int num_digits4(int r) { return r <= 1 ? 0 : 1 + num_digits4((r + 3) / 4); }
 constexpr int pow4(int i) { return i == 0 ? 1 : 4 * pow4(i - 1); }
 
+// The twiddle mode of stage (NS, R): mode 3 applies to the small stage
+// tables and falls back to mode 1 for the others.
+template <class K, int NS, int R>
+constexpr int stage_twmode() {
+    return K::TWMODE != 3 ? K::TWMODE : (lds_tw_stage(NS, R) ? 3 : 1);
+}
+
 template <class K, int NS, int R>
 struct TwRegs {
     static constexpr int B = K::P / R;
+    static constexpr int MODE = stage_twmode<K, NS, R>();
     // With the per-stage tables, the R - 1 factors of every butterfly would
     // all be live across the exchange: 60 VGPRs at radix 16 with two
     // butterflies per thread, 62 at radix 32, either of which spills.  Those
     // stages read each butterfly's factors just before applying them instead.
-    static constexpr bool LATE = K::TWMODE == 2 && (B > 1 || R >= 32);
-    static constexpr int LOADS = NS == 1 || LATE ? 0 : (K::TWMODE == 1 ? num_digits4(R) : R - 1);
+    static constexpr bool LATE = MODE == 2 && (B > 1 || R >= 32);
+    static constexpr int LOADS = NS == 1 || LATE || MODE == 3 ? 0 : (MODE == 1 ? num_digits4(R) : R - 1);
     float2 w[B][LOADS > 0 ? LOADS : 1];
 };
 
@@ -170,12 +208,12 @@ __device__ __forceinline__ void tw_issue(TwRegs<K, NS, R> &tr, int t, const floa
         static_for<0, B>([&](auto qc) {
             constexpr int q = decltype(qc)::value;
             const int k = (t + q * T) & (NS - 1);
-            if constexpr (K::TWMODE == 0) {
+            if constexpr (TwRegs<K, NS, R>::MODE == 0) {
                 static_for<1, R>([&](auto rc) {
                     constexpr int r = decltype(rc)::value;
                     tr.w[q][r - 1] = tw[k * (r * STR)];
                 });
-            } else if constexpr (K::TWMODE == 2) {
+            } else if constexpr (TwRegs<K, NS, R>::MODE == 2) {
                 // this stage's own table: row r - 1 holds W_(NS R)^(k r) at
                 // column k, so consecutive lanes read consecutive entries
                 constexpr long long OFF = stage_table_offset(K::N, NS, R);
@@ -204,7 +242,7 @@ __device__ __forceinline__ void tw_issue(TwRegs<K, NS, R> &tr, int t, const floa
 template <class K, int NS, int R, int q, bool INV>
 __device__ __forceinline__ void tw_apply(const TwRegs<K, NS, R> &tr, float2 (&u)[R]) {
     auto mul = [](float2 a, float2 w) { return INV ? cmulc(a, w) : cmul(a, w); };
-    if constexpr (K::TWMODE != 1) {
+    if constexpr (TwRegs<K, NS, R>::MODE != 1) {
         static_for<1, R>([&](auto rc) { u[rc] = mul(u[rc], tr.w[q][rc - 1]); });
     } else {
         constexpr int D = TwRegs<K, NS, R>::LOADS;
@@ -331,7 +369,17 @@ __device__ __forceinline__ void run_stages(float2 (&v)[K::P], int t, int c, cons
         constexpr int q = decltype(qc)::value;
         float2 u[R];
         static_for<0, R>([&](auto rc) { u[rc] = v[q + rc * B]; });
-        if constexpr (NS > 1 && TwRegs<K, NS, R>::LATE) {
+        if constexpr (NS > 1 && TwRegs<K, NS, R>::MODE == 3) {
+            // this butterfly's factors from the LDS copy of the stage table
+            // (row r - 1, column k: consecutive lanes, consecutive entries)
+            const float2 *L = reinterpret_cast<const float2 *>(lds + K::TWL_OFF) + lds_tw_offset(typename K::Rad{}, NS);
+            const int k = (t + q * K::T) & (NS - 1);
+            static_for<1, R>([&](auto rc) {
+                constexpr int r = decltype(rc)::value;
+                const float2 w = L[(r - 1) * NS + k];
+                u[r] = INV ? cmulc(u[r], w) : cmul(u[r], w);
+            });
+        } else if constexpr (NS > 1 && TwRegs<K, NS, R>::LATE) {
             // this butterfly's factors from the stage table, read now
             constexpr long long OFF = stage_table_offset(K::N, NS, R);
             const int k = (t + q * K::T) & (NS - 1);
@@ -354,6 +402,44 @@ __device__ __forceinline__ void run_stages(float2 (&v)[K::P], int t, int c, cons
         run_stages<K, INV, false, NS2, Rest...>(v, t, c, tw, lds, nxt);
     }
 }
+
+// Twiddle mode 3: the workgroup copies the small stage tables into LDS.  Each
+// thread loads its share into registers before it issues its data loads and
+// writes them to LDS after, so the table reads overlap the data's latency;
+// the first reads of the copy come after the first exchange's barrier.
+template <class K, int NS, int... Rs>
+struct LdsTwFill {
+    __device__ __forceinline__ void load(const float2 *__restrict__) {}
+    __device__ __forceinline__ void store(float *) const {}
+};
+template <class K, int NS, int R, int... Rs>
+struct LdsTwFill<K, NS, R, Rs...> {
+    static constexpr int CNT = lds_tw_stage(NS, R) ? (R - 1) * NS : 0;
+    static constexpr int PER = (CNT + K::THREADS - 1) / K::THREADS;
+    float2 w[PER > 0 ? PER : 1];
+    LdsTwFill<K, NS * R, Rs...> rest;
+    __device__ __forceinline__ void load(const float2 *__restrict__ tw) {
+        static_for<0, PER>([&](auto pc) {
+            const int i = decltype(pc)::value * K::THREADS + (int)threadIdx.x;
+            if (i < CNT) w[pc] = tw[stage_table_offset(K::N, NS, R) + i];
+        });
+        rest.load(tw);
+    }
+    __device__ __forceinline__ void store(float *lds) const {
+        float2 *L = reinterpret_cast<float2 *>(lds + K::TWL_OFF) + lds_tw_offset(typename K::Rad{}, NS);
+        static_for<0, PER>([&](auto pc) {
+            const int i = decltype(pc)::value * K::THREADS + (int)threadIdx.x;
+            if (i < CNT) L[i] = w[pc];
+        });
+        rest.store(lds);
+    }
+};
+template <class K, class Rad>
+struct LdsTwFillOf;
+template <class K, int... Rs>
+struct LdsTwFillOf<K, Radices<Rs...>> {
+    using type = LdsTwFill<K, 1, Rs...>;
+};
 
 template <class K, bool INV, bool FIRST_X, int R1, int... Rs>
 __device__ __forceinline__ void run_fft(Radices<R1, Rs...>, float2 (&v)[K::P], int t, int c,
@@ -821,6 +907,9 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
         constexpr int GROUP = EPI == EPI_RCMC && LINE_GROUP < 8 ? 8 : LINE_GROUP;
         const long long blk = logical_block<GROUP>(a.xcd_remap);
         const bool valid = blk * K::C + c < a.batch;
+        static_assert(K::TWL == 0 || EPI != EPI_RCMC, "the migration pass keeps its taps in LDS");
+        [[maybe_unused]] typename LdsTwFillOf<K, typename K::Rad>::type twl;
+        if constexpr (K::TWL > 0) twl.load(tw);
         if constexpr (EPI == EPI_SCALE) {
             // the range-Doppler chain's tables for the migration pass that follows
             if (a.rd_tables)
@@ -834,6 +923,7 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
             if constexpr (PRIO) __builtin_amdgcn_s_setprio(3);
             load_points<K, IN_ST>(v, in, blk, c, t, valid, a);
             if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
+            if constexpr (K::TWL > 0) twl.store(lds);
             if constexpr (EPI == EPI_MATCHED_Y) {
                 transform<K, INV, EPI, true>(v, t, c, tw, spec, a.scale, lds, (int)blockIdx.y, a.spec_shift);
             } else {
