@@ -562,10 +562,12 @@ def kernel_label(name: str) -> str:
                   r"mi355fft::Radices<([\d, ]+)>, (true|false)>, (\d), (\d), (true|false), (\d)>", name)
     if not m:
         return name.split("(")[0].replace("void ", "")[:80]
-    n, p, c, cols, xchg, _tw, pers, rad, _nt, ist, ost, inv, epi = m.groups()
+    n, p, c, cols, xchg, tw, pers, rad, _nt, ist, ost, inv, epi = m.groups()
     st = {"0": "fp32", "1": "fp16"}
+    # twiddle mode 1 (digit-base products, the common case) is not named
+    twn = {"0": " tw=table", "2": " tw=stage-tables", "3": " tw=lds-tables"}.get(tw, "")
     return (f"N={n} {'cols' if cols == 'true' else 'rows'} C={c} P={p} {XCHG_NAMES.get(int(xchg), xchg)} "
-            f"[{rad.replace(' ', '')}]{' persistent' if pers == 'true' else ''} "
+            f"[{rad.replace(' ', '')}]{twn}{' persistent' if pers == 'true' else ''} "
             f"{EPI_NAMES.get(int(epi), epi)} {st[ist]}->{st[ost]}{' inv' if inv == 'true' else ''}")
 
 
