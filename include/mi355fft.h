@@ -187,8 +187,10 @@ int fft_plan_destroy(fft_plan *plan);
 
 /*
  * sar_workspace_bytes -- device workspace sar_form_image_ex needs.
- * Holds both reference spectra and the range-compressed intermediate image
- * (n_az * n_rg * 8 bytes for FP32, * 4 bytes for FP16 intermediates).
+ * Holds both reference spectra, a 256-byte slot for the flag with which the
+ * range pass publishes the range spectrum to its own workgroups, and the
+ * range-compressed intermediate image (n_az * n_rg * 8 bytes for FP32, * 4
+ * bytes for FP16 intermediates).
  * Returns 0 for an invalid or unsupported request.
  */
 size_t sar_workspace_bytes(int64_t n_az, int64_t n_rg, int inter_storage);
@@ -210,11 +212,15 @@ size_t sar_workspace_bytes(int64_t n_az, int64_t n_rg, int inter_storage);
  *                   raw or the workspace.
  *   workspace       sar_workspace_bytes(n_az, n_rg, inter_storage) bytes,
  *                   256-byte aligned; contents on entry are ignored.
- *   stream          HIP stream; three kernels are launched on it in order
- *                   (five for n_az of 8192 or 16384 with FP32 intermediates,
- *                   whose azimuth pass runs as three passes of short columns;
- *                   `out` then also holds the range-compressed image between
- *                   the passes).
+ *   stream          HIP stream; two kernels are launched on it in order when
+ *                   n_az == n_rg: the range pass, whose first workgroups
+ *                   compute both reference spectra, and the azimuth pass.
+ *                   Otherwise the azimuth reference spectrum takes a launch
+ *                   of its own first (three).  For n_az of 8192 or 16384
+ *                   with FP32 intermediates the azimuth pass runs as three
+ *                   passes of short columns after a launch of both spectra
+ *                   (five; `out` then also holds the range-compressed image
+ *                   between the passes).
  *
  * Computes, with H_r = FFT(range_ref) and H_a = FFT(az_ref):
  *   y[a, :]   = IFFT( FFT(raw[a, :]) * conj(H_r) ) / n_rg      (pass 1, rows)
@@ -277,7 +283,8 @@ typedef struct sar_geometry {
 
 /*
  * sar_rd_workspace_bytes -- device workspace sar_rd_form_image needs: the
- * range reference spectrum, the per-Doppler-bin and per-range-bin tables of
+ * range reference spectrum, a 256-byte flag slot (as in sar_workspace_bytes),
+ * the per-Doppler-bin and per-range-bin tables of
  * the migration correction and azimuth filter, the interpolator table and
  * one intermediate image (the range-Doppler image, stored one row per range
  * bin: n_az * n_rg * 8 bytes for FP32, * 4 for FP16), each part 256-byte
@@ -314,8 +321,10 @@ size_t sar_rd_workspace_bytes(int64_t n_az, int64_t n_rg, int inter_storage);
  *                   the first two passes.
  *   workspace       sar_rd_workspace_bytes(n_az, n_rg, inter_storage) bytes,
  *                   256-byte aligned; contents on entry are ignored.
- *   stream          HIP stream; five kernels run on it in order (tables,
- *                   reference spectrum, three passes).
+ *   stream          HIP stream; three kernels run on it in order: the range
+ *                   pass (its workgroup 0 computes the reference spectrum),
+ *                   the azimuth FFT (which also fills the migration tables)
+ *                   and the migration-correction pass.
  *
  * Computes, in Section X's order:
  *   1. y[a, :] = IFFT( FFT(raw[a, :]) * conj(FFT(range_ref)) ) / n_rg;

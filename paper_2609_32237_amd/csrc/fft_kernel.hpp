@@ -798,6 +798,25 @@ __device__ __forceinline__ void store_remapped(float2 (&v)[K::P], void *__restri
     }
 }
 
+// An image row of a range pass whose reference spectrum workgroup 0 of the
+// same launch computes waits for it before reading the spectrum.  Workgroup 0
+// is dispatched first and waits for nothing, so the flag gets set; the bound
+// (about a second of polling) only keeps a kernel from spinning forever should
+// that ever fail.  One thread polls with agent-scope loads; the barrier then
+// orders the workgroup's spectrum reads after the flag was seen.  No cache
+// can hold an older copy of the spectrum: the launch starts with L1 and L2
+// invalidated, and nothing in it reads the spectrum before it is published,
+// so no acquire invalidation (of the whole L2, once per workgroup) is needed.
+__device__ __forceinline__ void wait_for_reference(unsigned long long *flag, unsigned long long epoch) {
+    if (threadIdx.x == 0) {
+        for (int n = 0; n < (1 << 22); ++n) {
+            if (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == epoch) break;
+            __builtin_amdgcn_s_sleep(8);
+        }
+    }
+    __syncthreads();
+}
+
 // The whole on-chip computation of one transform (first exchange of the
 // kernel may skip its leading barrier).
 // t and c are the caller's lane coordinates; the fused inverse launders them
@@ -805,7 +824,8 @@ __device__ __forceinline__ void store_remapped(float2 (&v)[K::P], void *__restri
 template <class K, bool INV, int EPI, bool FIRST_X>
 __device__ __forceinline__ void transform(float2 (&v)[K::P], int &t, int &c, const float2 *__restrict__ tw,
                                           const float2 *__restrict__ spec, float scale, float *lds,
-                                          int spec_off = 0, int spec_shift = 0) {
+                                          int spec_off = 0, int spec_shift = 0,
+                                          unsigned long long *ref_flag = nullptr, unsigned long long ref_epoch = 0) {
     constexpr bool MF = EPI == EPI_MATCHED || EPI == EPI_MATCHED_Y;
     if constexpr (K::XCHG == XCHG_LANE) {
         static_assert(EPI == EPI_NONE, "the cross-lane kernels run plain transforms");
@@ -820,6 +840,10 @@ __device__ __forceinline__ void transform(float2 (&v)[K::P], int &t, int &c, con
         // at a time between fences, so it never needs a second register
         // array beside X.
         __builtin_amdgcn_sched_barrier(0);
+        if constexpr (EPI == EPI_MATCHED && !K::COLS) {
+            // the spectrum is being computed by workgroup 0 of this launch
+            if (ref_flag) wait_for_reference(ref_flag, ref_epoch);
+        }
         // (the chains fold their power-of-two 1/N into the spectrum, which is
         // exact, so no scale is applied here)
         constexpr int HC = K::P < 8 ? K::P : 8;
@@ -859,6 +883,45 @@ __device__ __forceinline__ void transform(float2 (&v)[K::P], int &t, int &c, con
     }
 }
 
+// The reference spectra of a SAR chain (Section X: H_r and H_a, the range
+// and azimuth reference chirps' transforms), computed by the first
+// workgroups of its range pass rather than by a launch of their own.  Thread
+// (blk, c) transforms reference row r = blk * C + c (lanes past the last row
+// transform row 0 again and store nothing).  Workgroup 0 holds row 0, the
+// range spectrum that the image rows multiply by: once every thread's stores
+// have completed, one thread writes this XCD's L2 back (agent-scope release
+// fence), waits for that, and stores the call's epoch to the flag.
+template <class K>
+__device__ __forceinline__ void reference_rows(float2 (&v)[K::P], long long blk, int c, int t,
+                                               const float2 *__restrict__ tw, const KArgs &a, float *lds) {
+    const int r = (int)blk * K::C + c;
+    const bool mine = r < a.ref_rows;
+    const bool second = mine && r == 1;
+    const float2 *src = second ? a.ref_in[1] : a.ref_in[0];
+    [[maybe_unused]] typename LdsTwFillOf<K, typename K::Rad>::type twl;
+    if constexpr (K::TWL > 0) twl.load(tw);
+    static_for<0, K::P>([&](auto ic) { v[ic] = src[t + K::T * decltype(ic)::value]; });
+    if constexpr (K::TWL > 0) twl.store(lds);
+    int tt = t, cc = c;
+    transform<K, false, EPI_NONE, true>(v, tt, cc, tw, nullptr, second ? a.ref_scale[1] : a.ref_scale[0], lds);
+    if (mine) {
+        float2 *dst = second ? a.ref_out[1] : a.ref_out[0];
+        static_for<0, K::P>([&](auto ic) { dst[t + K::T * decltype(ic)::value] = v[ic]; });
+    }
+    if (blk == 0) {
+        __builtin_amdgcn_s_waitcnt(0);  // this thread's stores have reached L2
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            // write this XCD's L2 back, wait until that has completed, then
+            // publish (the explicit wait keeps the flag from overtaking the
+            // write-back)
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+            __builtin_amdgcn_s_waitcnt(0);
+            __hip_atomic_store(a.ref_flag, a.ref_epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+}
+
 // Occupancy hint: the LDS-derived minimum, except for persistent kernels,
 // which hold a second transform and need more registers than that leaves.
 template <class K, int EPI>
@@ -891,6 +954,7 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
         in = reinterpret_cast<const char *>(in) + in_off * Store<IN_ST>::BYTES;
         out = reinterpret_cast<char *>(out) + out_off * Store<OUT_ST>::BYTES;
     }
+    if (a.clear_flag && (blockIdx.x | blockIdx.y | blockIdx.z | threadIdx.x) == 0) *a.clear_flag = 0ull;
     const int tid = threadIdx.x;
     int c = K::COLS ? (tid & (K::C - 1)) : (tid >> K::LOG_T);
     int t = K::COLS ? (tid >> K::LOG_C) : (tid & (K::T - 1));
@@ -905,7 +969,18 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
                                                                                 : Store<OUT_ST>::BYTES);
         constexpr int LINE_GROUP = PIECE >= 128 ? 1 : 128 / PIECE;
         constexpr int GROUP = EPI == EPI_RCMC && LINE_GROUP < 8 ? 8 : LINE_GROUP;
-        const long long blk = logical_block<GROUP>(a.xcd_remap);
+        long long blk = logical_block<GROUP>(a.xcd_remap);
+        if constexpr (EPI == EPI_MATCHED && !K::COLS) {
+            if (a.ref_blocks > 0) {
+                // the chain's reference spectra come first (the launcher
+                // keeps blocks in dispatch order for them)
+                if (blk < a.ref_blocks) {
+                    reference_rows<K>(v, blk, c, t, tw, a, lds);
+                    return;
+                }
+                blk -= a.ref_blocks;
+            }
+        }
         const bool valid = blk * K::C + c < a.batch;
         static_assert(K::TWL == 0 || EPI != EPI_RCMC, "the migration pass keeps its taps in LDS");
         [[maybe_unused]] typename LdsTwFillOf<K, typename K::Rad>::type twl;
@@ -927,7 +1002,7 @@ void fft_kernel(const void *__restrict__ in, void *__restrict__ out,
             if constexpr (EPI == EPI_MATCHED_Y) {
                 transform<K, INV, EPI, true>(v, t, c, tw, spec, a.scale, lds, (int)blockIdx.y, a.spec_shift);
             } else {
-                transform<K, INV, EPI, true>(v, t, c, tw, spec, a.scale, lds);
+                transform<K, INV, EPI, true>(v, t, c, tw, spec, a.scale, lds, 0, 0, a.ref_flag, a.ref_epoch);
             }
         }
         if constexpr (EPI == EPI_TWIDDLE || EPI == EPI_TWIDDLE_Y || EPI == EPI_MATCHED_Y) {
@@ -1023,6 +1098,17 @@ hipError_t launch_one(const void *in, void *out, const float2 *tw, const float2 
     set_spans(a, K::N, K::C, Store<IN_ST>::BYTES, Store<OUT_ST>::BYTES);
     long long blocks = (a.batch + K::C - 1) / K::C;
     if (blocks <= 0 || blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+    a.ref_blocks = 0;
+    if (a.ref_rows > 0) {
+        // reference rows ahead of the image rows: matched rows only, blocks
+        // in dispatch order, one problem; hipErrorNotSupported tells the
+        // caller to run the reference transforms as a launch of their own
+        constexpr bool OK = EPI == EPI_MATCHED && !K::COLS && !K::PERSIST && K::XCHG != XCHG_LANE;
+        if (!OK || a.ref_rows > 2 || !a.ref_flag || a.xcd_remap != XCD_NONE || a.outer > 1 || a.outer2 > 1)
+            return hipErrorNotSupported;
+        a.ref_blocks = (a.ref_rows + K::C - 1) / K::C;
+        blocks += a.ref_blocks;
+    }
     auto kern = fft_kernel<K, IN_ST, OUT_ST, INV, EPI>;
     if constexpr (K::PERSIST) {
         static std::atomic<int> resident{0};  // workgroups resident on the whole device

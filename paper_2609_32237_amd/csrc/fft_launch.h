@@ -159,6 +159,25 @@ struct KArgs {
     RdGeometry rd_geo;
     const float2 *rd_interp;
     void *rd_tables;
+    // EPI_MATCHED rows: the chain's reference spectra computed by the first
+    // workgroups of the range pass instead of a launch of their own.
+    // Reference row r < ref_rows (r = 0 the range reference, whose spectrum
+    // is `spec`; r = 1 the azimuth reference) is ref_in[r] (FP32, N points,
+    // contiguous), transformed forward, times ref_scale[r], stored to
+    // ref_out[r] (FP32).  It belongs to thread (blk, c) with blk * C + c = r;
+    // the image rows follow as blocks ref_blocks .. (set by the launcher).
+    // Workgroup 0 then stores ref_epoch to *ref_flag (agent-scope release)
+    // and each image workgroup waits for that value before it reads `spec`.
+    int ref_rows;
+    int ref_blocks;
+    const float2 *ref_in[2];
+    float2 *ref_out[2];
+    float ref_scale[2];
+    unsigned long long *ref_flag;
+    unsigned long long ref_epoch;
+    // Any kernel: workgroup 0 first stores 0 to *clear_flag (a pass that
+    // runs after the one that waited on it, so no reader remains).
+    unsigned long long *clear_flag;
 };
 
 // Fills the addressing fields of `a` for workgroups of `c` transforms of `n`

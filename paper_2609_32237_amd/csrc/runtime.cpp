@@ -6,12 +6,15 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
+#include <chrono>
 #include <cmath>
 #include <cstdint>
 #include <cstdlib>
 #include <map>
 #include <mutex>
 #include <new>
+#include <random>
 #include <utility>
 #include <vector>
 
@@ -369,7 +372,29 @@ constexpr int64_t kMaxRdPoints = int64_t(1) << 27;
 constexpr double kMaxDopplerRatio = 1.0 / 3.0;  // 15 (1 / sqrt(1 - 1/9) - 1) = 0.91
 
 // Workspace of sar_rd_form_image: range reference spectrum, tables, image.
-size_t rd_tables_offset(int64_t n_rg) { return (size_t)n_rg * sizeof(float2); }  // n_rg >= 1024: 256-aligned
+// Every chain workspace holds one 256-byte slot for the flag with which the
+// range pass's workgroup 0 publishes the range reference spectrum.
+constexpr size_t kChainFlagBytes = 256;
+
+// A fresh value per chain call for that flag: 64 bits from a per-process
+// random start, never 0 (the value the pass after the range pass leaves), so
+// neither a stale flag of an earlier call nor uninitialised workspace memory
+// reads as this call's.
+unsigned long long next_chain_epoch() {
+    static std::atomic<unsigned long long> counter{[] {
+        std::random_device rd;
+        const unsigned long long t = (unsigned long long)std::chrono::steady_clock::now().time_since_epoch().count();
+        return (((unsigned long long)rd() << 32) ^ (unsigned long long)rd()) ^ (t * 0x9E3779B97F4A7C15ull);
+    }()};
+    unsigned long long e = counter.fetch_add(1, std::memory_order_relaxed);
+    if (e == 0) e = counter.fetch_add(1, std::memory_order_relaxed);
+    return e;
+}
+
+// range-Doppler workspace: H_r, the flag slot, the migration tables, the
+// transposed range-Doppler image
+size_t rd_flag_offset(int64_t n_rg) { return (size_t)n_rg * sizeof(float2); }
+size_t rd_tables_offset(int64_t n_rg) { return rd_flag_offset(n_rg) + kChainFlagBytes; }  // n_rg >= 1024: 256-aligned
 size_t rd_mid_offset(int64_t n_az, int64_t n_rg) {
     return rd_tables_offset(n_rg) + (size_t)mi355fft::rd_tables_layout(n_az, n_rg).bytes;
 }
@@ -661,7 +686,7 @@ size_t sar_workspace_bytes(int64_t n_az, int64_t n_rg, int inter_storage) {
     if (inter_storage != FFT_STORAGE_FP32 && inter_storage != FFT_STORAGE_FP16) return 0;
     const size_t spectra = (size_t)(n_az + n_rg) * sizeof(float2);  // multiple of 256 bytes
     const size_t el = inter_storage == FFT_STORAGE_FP32 ? 8 : 4;
-    return spectra + (size_t)n_az * (size_t)n_rg * el;
+    return spectra + kChainFlagBytes + (size_t)n_az * (size_t)n_rg * el;
 }
 
 // An azimuth pass over 8192- or 16384-point columns holds one or two columns
@@ -756,7 +781,8 @@ int sar_run(int64_t n_az, int64_t n_rg, int inter_storage, const void *raw, cons
 
     float2 *h_rg = reinterpret_cast<float2 *>(workspace);
     float2 *h_az = h_rg + n_rg;
-    void *mid = h_az + n_az;
+    auto *flag = reinterpret_cast<unsigned long long *>(h_az + n_az);
+    void *mid = reinterpret_cast<char *>(flag) + kChainFlagBytes;
     using mi355fft::EPI_MATCHED;
     using mi355fft::EPI_NONE;
     using mi355fft::LAYOUT_COLS;
@@ -765,36 +791,71 @@ int sar_run(int64_t n_az, int64_t n_rg, int inter_storage, const void *raw, cons
 
     // reference spectra into the workspace, each with its pass's scale folded
     // in (a power of two, so exact): H_r / n_rg and H_a / n_az; the passes
-    // multiply by their conjugates.  Equal lengths: one launch of two
-    // transforms (the input distance is the signed distance between the two
-    // reference buffers).
+    // multiply by their conjugates.
     const float s_rg = (float)(1.0 / (double)n_rg), s_az = (float)(1.0 / (double)n_az);
-    if (n_rg == n_az) {
-        const long long gap = ((const char *)az_ref - (const char *)range_ref) / (long long)sizeof(float2);
-        const KArgs a{2, 1, gap, n_rg, s_rg, 0};
-        e = launch_fft(n_rg, vrow, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, range_ref, h_rg, t.tw_rg, nullptr, a, stream);
-        if (e != hipSuccess) return map_hip(e);
-    } else {
-        const KArgs a1{1, 1, n_rg, n_rg, s_rg, 0};
-        e = launch_fft(n_rg, vrow, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, range_ref, h_rg, t.tw_rg, nullptr, a1, stream);
-        if (e != hipSuccess) return map_hip(e);
-        const KArgs a2{1, 1, n_az, n_az, s_az, 0};
-        e = launch_fft(n_az, vref, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, az_ref, h_az, t.tw_az, nullptr, a2, stream);
-        if (e != hipSuccess) return map_hip(e);
-    }
+    auto separate_references = [&](bool range, bool azimuth) -> hipError_t {
+        hipError_t err = hipSuccess;
+        if (range && azimuth && n_rg == n_az) {
+            // one launch of two transforms (the input distance is the signed
+            // distance between the two reference buffers)
+            const long long gap = ((const char *)az_ref - (const char *)range_ref) / (long long)sizeof(float2);
+            const KArgs a{2, 1, gap, n_rg, s_rg, 0};
+            return launch_fft(n_rg, vrow, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, range_ref, h_rg, t.tw_rg, nullptr, a,
+                              stream);
+        }
+        if (range) {
+            const KArgs a1{1, 1, n_rg, n_rg, s_rg, 0};
+            err = launch_fft(n_rg, vrow, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, range_ref, h_rg, t.tw_rg, nullptr, a1, stream);
+            if (err != hipSuccess) return err;
+        }
+        if (azimuth) {
+            const KArgs a2{1, 1, n_az, n_az, s_az, 0};
+            err = launch_fft(n_az, vref, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, az_ref, h_az, t.tw_az, nullptr, a2, stream);
+        }
+        return err;
+    };
 
     if (long_azimuth(n_az, inter_storage)) {
+        e = separate_references(true, true);
+        if (e != hipSuccess) return map_hip(e);
         return sar_long_azimuth(n_az, n_rg, raw, out, mid, h_rg, h_az, t, vrow, stream);
     }
 
-    // pass 1, rows (range): FFT, * conj(H_r / n_rg), IFFT -> intermediate
-    const KArgs ar{n_az, 1, n_rg, n_rg, 1.0f, 0};
+    // pass 1, rows (range): FFT, * conj(H_r / n_rg), IFFT -> intermediate.
+    // Its first workgroups compute the reference spectra (both of them when
+    // the image is square, else H_r, with H_a a launch of its own), saving
+    // the launch that would precede the pass; a row shape that cannot hold
+    // them (persistent) falls back to that launch.
+    const bool square = n_az == n_rg;
+    if (!square) {
+        e = separate_references(false, true);
+        if (e != hipSuccess) return map_hip(e);
+    }
+    KArgs ar{n_az, 1, n_rg, n_rg, 1.0f, 0};
+    ar.ref_rows = square ? 2 : 1;
+    ar.ref_in[0] = reinterpret_cast<const float2 *>(range_ref);
+    ar.ref_out[0] = h_rg;
+    ar.ref_scale[0] = s_rg;
+    ar.ref_in[1] = reinterpret_cast<const float2 *>(az_ref);
+    ar.ref_out[1] = h_az;
+    ar.ref_scale[1] = s_az;
+    ar.ref_flag = flag;
+    ar.ref_epoch = next_chain_epoch();
     e = launch_fft(n_rg, vrow, LAYOUT_ROWS, FFT_STORAGE_FP32, inter_storage, 0, EPI_MATCHED, raw, mid, t.tw_rg, h_rg,
                    ar, stream);
+    if (e == hipErrorNotSupported) {
+        e = separate_references(true, square);
+        if (e != hipSuccess) return map_hip(e);
+        const KArgs ar2{n_az, 1, n_rg, n_rg, 1.0f, 0};
+        e = launch_fft(n_rg, vrow, LAYOUT_ROWS, FFT_STORAGE_FP32, inter_storage, 0, EPI_MATCHED, raw, mid, t.tw_rg,
+                       h_rg, ar2, stream);
+    }
     if (e != hipSuccess) return map_hip(e);
 
-    // pass 2, columns (azimuth): FFT, * conj(H_a / n_az), IFFT -> image
-    const KArgs ac{n_rg, n_rg, 1, 1, 1.0f, strip_map(n_rg * 8)};
+    // pass 2, columns (azimuth): FFT, * conj(H_a / n_az), IFFT -> image; it
+    // clears the flag the range pass waited on
+    KArgs ac{n_rg, n_rg, 1, 1, 1.0f, strip_map(n_rg * 8)};
+    ac.clear_flag = flag;
     e = launch_fft(n_az, vcol, LAYOUT_COLS, inter_storage, FFT_STORAGE_FP32, 0, EPI_MATCHED, mid, out, t.tw_az, h_az,
                    ac, stream);
     return map_hip(e);
@@ -812,9 +873,9 @@ constexpr size_t kNaTwBytes = na_tw_entries_below(32768) * sizeof(float2);  // l
 constexpr size_t kNaFtabOffset = kNaTwBytes;
 constexpr size_t kNaFtabBytes = (size_t)(192 + 256) * sizeof(float2);  // 8192: 128 + 64; 16384: 128 + 128
 constexpr size_t kNaWorkspaceOffset = mi355fft::round_up_256(kNaFtabOffset + kNaFtabBytes);
-static_assert(kNaWorkspaceOffset + 2 * 16384 * sizeof(float2) + mi355fft::kNoallocMaxImageBytes <=
+static_assert(kNaWorkspaceOffset + 2 * 16384 * sizeof(float2) + kChainFlagBytes + mi355fft::kNoallocMaxImageBytes <=
                   mi355fft::kNoallocScratchBytes,
-              "the fixed array holds the tables, both spectra and the largest intermediate");
+              "the fixed array holds the tables, both spectra, the flag and the largest intermediate");
 
 size_t na_tw_offset(int64_t n) { return na_tw_entries_below(n) * sizeof(float2); }
 size_t na_ftab_offset(int64_t n) { return kNaFtabOffset + (n == 8192 ? 0 : 192 * sizeof(float2)); }
@@ -960,15 +1021,31 @@ int sar_rd_form_image(int64_t n_az, int64_t n_rg, int inter_storage, const sar_g
     void *tables = wsb + rd_tables_offset(n_rg);
     void *zt = wsb + rd_mid_offset(n_az, n_rg);
 
-    const KArgs aref{1, 1, n_rg, n_rg, (float)(1.0 / (double)n_rg), 0};  // H_r / n_rg (exact)
-    e = launch_fft(n_rg, vrow, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, range_ref, h_rg, tw_rg, nullptr, aref, stream);
-    if (e != hipSuccess) return map_hip(e);
+    auto *flag = reinterpret_cast<unsigned long long *>(wsb + rd_flag_offset(n_rg));
+    const float s_rg = (float)(1.0 / (double)n_rg);  // H_r / n_rg (exact)
+
     // 1: range compression, rows: FFT, * conj(H_r) / n_rg, IFFT.  The
     //    range-compressed image is kept in `out`, which the last pass
-    //    overwrites with the focused image.  H_r carries the 1/n_rg.
-    const KArgs ar{n_az, 1, n_rg, n_rg, 1.0f, 0};
+    //    overwrites with the focused image.  H_r carries the 1/n_rg; the
+    //    pass's workgroup 0 computes it (a row shape that cannot falls back
+    //    to a launch of its own).
+    KArgs ar{n_az, 1, n_rg, n_rg, 1.0f, 0};
+    ar.ref_rows = 1;
+    ar.ref_in[0] = reinterpret_cast<const float2 *>(range_ref);
+    ar.ref_out[0] = h_rg;
+    ar.ref_scale[0] = s_rg;
+    ar.ref_flag = flag;
+    ar.ref_epoch = next_chain_epoch();
     e = launch_fft(n_rg, vrow, LAYOUT_ROWS, FFT_STORAGE_FP32, inter_storage, 0, EPI_MATCHED, raw, out, tw_rg, h_rg,
                    ar, stream);
+    if (e == hipErrorNotSupported) {
+        const KArgs aref{1, 1, n_rg, n_rg, s_rg, 0};
+        e = launch_fft(n_rg, vrow, LAYOUT_ROWS, 0, 0, 0, EPI_NONE, range_ref, h_rg, tw_rg, nullptr, aref, stream);
+        if (e != hipSuccess) return map_hip(e);
+        const KArgs ar2{n_az, 1, n_rg, n_rg, 1.0f, 0};
+        e = launch_fft(n_rg, vrow, LAYOUT_ROWS, FFT_STORAGE_FP32, inter_storage, 0, EPI_MATCHED, raw, out, tw_rg,
+                       h_rg, ar2, stream);
+    }
     if (e != hipSuccess) return map_hip(e);
     // 2: azimuth FFT of every range bin (a column), / n_az, written as one row
     //    per range bin (the transposed range-Doppler image)
@@ -979,6 +1056,7 @@ int sar_rd_form_image(int64_t n_az, int64_t n_rg, int inter_storage, const sar_g
     ab.rd_geo = RdGeometry{g[0], g[1], g[2], g[3], g[4]};
     ab.rd_interp = interp;
     ab.rd_tables = tables;
+    ab.clear_flag = flag;  // the range pass has finished: no reader remains
     e = launch_fft(n_az, vcol, LAYOUT_COLS, inter_storage, inter_storage, 0, EPI_SCALE, out, zt, tw_az, nullptr, ab,
                    stream);
     if (e != hipSuccess) return map_hip(e);

@@ -128,9 +128,10 @@ def test_sar_noalloc_argument_errors(L):
 
 
 def test_sar_workspace_bytes(L):
-    assert L.sar_workspace_bytes(4096, 4096, 0) == (4096 + 4096) * 8 + 4096 * 4096 * 8
-    assert L.sar_workspace_bytes(4096, 4096, 1) == (4096 + 4096) * 8 + 4096 * 4096 * 4
-    assert L.sar_workspace_bytes(1024, 16384, 1) == (1024 + 16384) * 8 + 1024 * 16384 * 4
+    # both spectra, the 256-byte flag slot of the range pass, the intermediate
+    assert L.sar_workspace_bytes(4096, 4096, 0) == (4096 + 4096) * 8 + 256 + 4096 * 4096 * 8
+    assert L.sar_workspace_bytes(4096, 4096, 1) == (4096 + 4096) * 8 + 256 + 4096 * 4096 * 4
+    assert L.sar_workspace_bytes(1024, 16384, 1) == (1024 + 16384) * 8 + 256 + 1024 * 16384 * 4
     assert L.sar_workspace_bytes(4096, 4000, 0) == 0
     assert L.sar_workspace_bytes(4096, 4096, 5) == 0
 
@@ -168,9 +169,9 @@ def test_sar_rd_workspace_bytes(L):
     def up(x):
         return (x + 255) // 256 * 256
     tables = up(4096 * 16) + up(4096 * 8) + up(129 * 8 * 8)
-    assert L.sar_rd_workspace_bytes(4096, 4096, 0) == 4096 * 8 + tables + 4096 * 4096 * 8
-    assert L.sar_rd_workspace_bytes(4096, 4096, 1) == 4096 * 8 + tables + 4096 * 4096 * 4
-    assert L.sar_rd_workspace_bytes(16384, 8192, 0) == 8192 * 8 + up(16384 * 16) + up(8192 * 8) + up(129 * 64) + \
+    assert L.sar_rd_workspace_bytes(4096, 4096, 0) == 4096 * 8 + 256 + tables + 4096 * 4096 * 8
+    assert L.sar_rd_workspace_bytes(4096, 4096, 1) == 4096 * 8 + 256 + tables + 4096 * 4096 * 4
+    assert L.sar_rd_workspace_bytes(16384, 8192, 0) == 8192 * 8 + 256 + up(16384 * 16) + up(8192 * 8) + up(129 * 64) + \
         16384 * 8192 * 8
     assert L.sar_rd_workspace_bytes(16384, 16384, 0) == 0  # beyond 2^27 points
     assert L.sar_rd_workspace_bytes(4096, 4000, 0) == 0

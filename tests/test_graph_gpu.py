@@ -85,3 +85,49 @@ def test_range_doppler_chain_in_a_graph(api):
     img = torch.empty_like(raw)
     ws = torch.empty(_lib.sar_rd_workspace_bytes(1024, 1024, 1), dtype=torch.uint8, device="cuda")
     replay_matches(lambda: api.sar_rd_form_image(raw, ref, sc.geometry, 1, out=img, workspace=ws), img)
+
+
+def test_square_sar_chain_in_a_graph_with_new_references(api):
+    """A square image's range pass computes both reference spectra in its
+    first workgroups and publishes the range spectrum to its own workgroups
+    through a flag in the workspace, which the azimuth pass clears.  Replays of
+    one captured chain (one flag value) with the references rewritten between
+    them must equal eager calls on the same inputs, bit for bit."""
+    import torch
+
+    from paper_2609_32237_amd import _lib
+
+    log("graph: square sar chain, references rewritten between replays")
+    n = 2048
+    sc1 = workloads.sar_scene(n_az=n, n_rg=n, n_targets=4, len_rg=256, beta_rg=0.8, len_az=128, beta_az=0.8,
+                              seed=78, min_sep=24)
+    sc2 = workloads.sar_scene(n_az=n, n_rg=n, n_targets=4, len_rg=320, beta_rg=0.6, len_az=96, beta_az=0.5,
+                              seed=78, min_sep=24)
+    raw, hr, ha = to_dev(sc1.raw), to_dev(sc1.range_ref), to_dev(sc1.az_ref)
+    refs = [(to_dev(sc1.range_ref), to_dev(sc1.az_ref)), (to_dev(sc2.range_ref), to_dev(sc2.az_ref))]
+    img = torch.empty_like(raw)
+    ws = torch.empty(_lib.sar_workspace_bytes(n, n, 0), dtype=torch.uint8, device="cuda")
+    s = torch.cuda.Stream()
+    expect = []
+    for r_rg, r_az in refs:
+        hr.copy_(r_rg)
+        ha.copy_(r_az)
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s):
+            api.sar_form_image(raw, hr, ha, 0, out=img, workspace=ws)
+        torch.cuda.synchronize()
+        expect.append(img.clone())
+    assert not torch.equal(expect[0], expect[1])
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        api.sar_form_image(raw, hr, ha, 0, out=img, workspace=ws)
+    torch.cuda.synchronize()
+    for rep in range(6):
+        k = rep % 2
+        hr.copy_(refs[k][0])
+        ha.copy_(refs[k][1])
+        img.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(img.view(torch.float32), expect[k].view(torch.float32)), rep

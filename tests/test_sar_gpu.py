@@ -118,3 +118,42 @@ def test_single_target_peak_value(api):
     np.testing.assert_allclose(peak.real, 0.75 * 1024 * 512, rtol=1e-5)
     assert abs(peak.imag) < 1e-5 * 0.75 * 1024 * 512
     assert np.unravel_index(np.argmax(np.abs(img)), img.shape) == (2000, 1500)
+
+
+def test_workspace_contents_and_reuse(api):
+    """The range pass publishes the range spectrum to its own workgroups
+    through a flag in the workspace (a per-call value, cleared by the azimuth
+    pass).  Whatever the workspace held before (zeros, all ones, random bytes,
+    the previous call's state for other references), every call equals a call
+    on a fresh workspace, bit for bit."""
+    import torch
+
+    from paper_2609_32237_amd import _lib
+
+    log("sar workspace contents and reuse")
+    n = 1024
+    scenes = [workloads.sar_scene(n_az=n, n_rg=n, n_targets=4, len_rg=128, beta_rg=0.8, len_az=96, beta_az=0.8,
+                                  seed=s, min_sep=24) for s in (91, 92)]
+    scenes[1] = workloads.sar_scene(n_az=n, n_rg=n, n_targets=4, len_rg=200, beta_rg=0.5, len_az=64,
+                                    beta_az=0.6, seed=92, min_sep=24)
+    dev = [(to_dev(sc.raw), to_dev(sc.range_ref), to_dev(sc.az_ref)) for sc in scenes]
+    nbytes = _lib.sar_workspace_bytes(n, n, 0)
+    expect = []
+    for raw, hr, ha in dev:
+        ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        expect.append(api.sar_form_image(raw, hr, ha, 0, workspace=ws).clone())
+    torch.cuda.synchronize()
+    for k, sc in enumerate(scenes):
+        ref = oracle.sar_chain(sc.raw, sc.range_ref, sc.az_ref)
+        assert rel(to_host(expect[k]).astype(np.complex128), ref) < TOL[0]
+    gen = torch.Generator(device="cuda").manual_seed(5)
+    fills = [torch.zeros(nbytes, dtype=torch.uint8, device="cuda"),
+             torch.full((nbytes,), 0xFF, dtype=torch.uint8, device="cuda"),
+             torch.randint(0, 256, (nbytes,), dtype=torch.uint8, device="cuda", generator=gen)]
+    for f, ws in enumerate(fills):
+        for rep in range(6):
+            k = (rep + f) % 2
+            raw, hr, ha = dev[k]
+            out = api.sar_form_image(raw, hr, ha, 0, workspace=ws)
+            torch.cuda.synchronize()
+            assert torch.equal(out.view(torch.float32), expect[k].view(torch.float32)), (f, rep)
