@@ -208,6 +208,7 @@ size_t sar_workspace_bytes(int64_t n_az, int64_t n_rg, int inter_storage);
  *   range_ref       n_rg complex FP32: the time-domain range reference (the
  *                   transmitted chirp, centred and wrapped to index t mod n_rg).
  *   az_ref          n_az complex FP32: the time-domain azimuth reference.
+ *                   Neither reference may overlap the workspace (FFT_EINVAL).
  *   out             n_az x n_rg complex FP32 focused image; must not overlap
  *                   raw or the workspace.
  *   workspace       sar_workspace_bytes(n_az, n_rg, inter_storage) bytes,
@@ -314,7 +315,8 @@ size_t sar_rd_workspace_bytes(int64_t n_az, int64_t n_rg, int inter_storage);
  *                   call returns.
  *   raw             n_az x n_rg complex FP32 echo, row-major, rows = pulses.
  *   range_ref       n_rg complex FP32: the transmitted pulse replica,
- *                   starting at index 0 (zero beyond the pulse).
+ *                   starting at index 0 (zero beyond the pulse); must not
+ *                   overlap `out` or the workspace (FFT_EINVAL).
  *   out             n_az x n_rg complex FP32 focused image (rows = pulses,
  *                   columns = range bins); must not overlap raw or the
  *                   workspace.  Also holds the range-compressed image between

@@ -928,6 +928,9 @@ int sar_form_image_ex(int64_t n_az, int64_t n_rg, int inter_storage, const void 
     const size_t img = (size_t)n_az * (size_t)n_rg * 8;
     const size_t ws = sar_workspace_bytes(n_az, n_rg, inter_storage);
     if (overlaps(out, img, workspace, ws) || overlaps(raw, img, workspace, ws)) return FFT_EINVAL;
+    // the range pass reads the references while it writes the spectra
+    if (overlaps(range_ref, (size_t)n_rg * 8, workspace, ws) || overlaps(az_ref, (size_t)n_az * 8, workspace, ws))
+        return FFT_EINVAL;
 
     int device = 0;
     hipError_t e = hipGetDevice(&device);
@@ -960,6 +963,8 @@ int sar_form_image_noalloc(int64_t n_az, int64_t n_rg, int inter_storage, const 
     const size_t img = (size_t)n_az * (size_t)n_rg * 8;
     const size_t wsb = sar_workspace_bytes(n_az, n_rg, inter_storage);
     if (overlaps(out, img, ws, wsb) || overlaps(raw, img, ws, wsb)) return FFT_EINVAL;
+    if (overlaps(range_ref, (size_t)n_rg * 8, ws, wsb) || overlaps(az_ref, (size_t)n_az * 8, ws, wsb))
+        return FFT_EINVAL;
     auto tw = [&](int64_t n) { return reinterpret_cast<const float2 *>(base + na_tw_offset(n)); };
     SarTables t{tw(n_rg), tw(n_az), nullptr, nullptr, nullptr};
     if (long_azimuth(n_az, inter_storage)) {
@@ -997,6 +1002,9 @@ int sar_rd_form_image(int64_t n_az, int64_t n_rg, int inter_storage, const sar_g
     const size_t img = (size_t)n_az * (size_t)n_rg * 8;
     const size_t ws = sar_rd_workspace_bytes(n_az, n_rg, inter_storage);
     if (overlaps(out, img, raw, img) || overlaps(out, img, workspace, ws) || overlaps(raw, img, workspace, ws))
+        return FFT_EINVAL;
+    // the range pass reads the reference while it writes `out` and the spectrum
+    if (overlaps(range_ref, (size_t)n_rg * 8, workspace, ws) || overlaps(range_ref, (size_t)n_rg * 8, out, img))
         return FFT_EINVAL;
 
     int device = 0;

@@ -108,6 +108,10 @@ def test_sar_argument_errors(L):
     assert f(4096, 4096, 0, ok, ok, ok, 1 << 40, (1 << 41) + 8, None) == L.FFT_EALIGN  # workspace 256 B
     # out overlapping raw
     assert f(4096, 4096, 0, 1 << 30, ok, ok, (1 << 30) + 4096, 1 << 40, None) == L.FFT_EINVAL
+    # a reference inside the workspace (the range pass writes the spectra there)
+    ws = 1 << 41
+    assert f(4096, 4096, 0, 1 << 30, ws + 8, ok, 1 << 40, ws, None) == L.FFT_EINVAL
+    assert f(4096, 4096, 0, 1 << 30, ok, ws + (1 << 20), 1 << 40, ws, None) == L.FFT_EINVAL
     assert L.lib.sar_form_image(None, ok, ok, ok, None) == L.FFT_EINVAL
 
 
@@ -200,6 +204,8 @@ def test_sar_rd_argument_errors(L):
     assert f(4096, 4096, 0, g, ok, ok, 1 << 36, ws + 8, None) == L.FFT_EALIGN       # workspace 256 B
     assert f(4096, 4096, 0, g, 1 << 30, ok, (1 << 30) + 4096, ws, None) == L.FFT_EINVAL  # out overlaps raw
     assert f(4096, 4096, 0, g, ok, ok, ws + 4096, ws, None) == L.FFT_EINVAL         # out inside workspace
+    assert f(4096, 4096, 0, g, ok, ws + 256, 1 << 36, ws, None) == L.FFT_EINVAL     # reference inside workspace
+    assert f(4096, 4096, 0, g, ok, (1 << 36) + 64, 1 << 36, ws, None) == L.FFT_EINVAL  # reference inside out
 
 
 def test_long_transform_plans_are_accepted(L):
