@@ -173,12 +173,17 @@ struct Configs<16384> {
                        KCfg<16384, 32, 1, false, XCHG_SPLIT, 1, true, Radices<16, 16, 16, 4>>,
                        KCfg<16384, 32, 1, false, XCHG_SPLIT, 0, false, Radices<16, 16, 16, 4>>,
                        KCfg<16384, 32, 1, false, XCHG_SPLIT, 1, false, Radices<32, 16, 32>>,
-                       KCfg<16384, 32, 1, false, XCHG_SPLIT, 2, false, Radices<32, 16, 32>>>;
+                       KCfg<16384, 32, 1, false, XCHG_SPLIT, 2, false, Radices<32, 16, 32>>,
+                       // the second stage's 240 factors from LDS (twiddle mode 3)
+                       KCfg<16384, 16, 1, false, XCHG_SPLIT, 3, false, Radices<16, 16, 16, 4>>>;
     using Cols = KList<KCfg<16384, 32, 1, true, XCHG_SPLIT, 0, false, Radices<16, 16, 16, 4>>,
                        KCfg<16384, 32, 1, true, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 4>>>;
     // three stages (32 x 16 x 32) against four: one exchange and one twiddle
-    // pass fewer; measured 5.5 vs 5.3 TB/s (FP32) and 4.9 vs 3.8 TB/s (FP16)
-    static constexpr int kRowDefault[2] = {4, 4}, kColDefault[2] = {1, 1};
+    // pass fewer; measured 5.5 vs 5.3 TB/s (FP32) and 4.9 vs 3.8 TB/s (FP16).
+    // FP32: four stages with the second stage's factors from LDS beat both,
+    // 5,800-5,816 against 5,660-5,693 GB/s flushed and 5,637-5,828 against
+    // 5,128-5,722 back to back (two boxes, same process each)
+    static constexpr int kRowDefault[2] = {6, 4}, kColDefault[2] = {1, 1};
     using Rcmc = KList<KCfg<16384, 32, 2, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 4>>,
                        KCfg<16384, 16, 1, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16, 4>>>;
     // binary16 exchange: three stages fastest (4.8 TB/s), then 32 points per
