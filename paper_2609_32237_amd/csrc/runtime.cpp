@@ -382,9 +382,15 @@ constexpr size_t kChainFlagBytes = 256;
 // reads as this call's.
 unsigned long long next_chain_epoch() {
     static std::atomic<unsigned long long> counter{[] {
-        std::random_device rd;
+        unsigned long long r = 0;
+        try {  // no exception may leave the C ABI: without an entropy source, the clock alone
+            std::random_device rd;
+            r = ((unsigned long long)rd() << 32) ^ (unsigned long long)rd();
+        } catch (...) {
+        }
         const unsigned long long t = (unsigned long long)std::chrono::steady_clock::now().time_since_epoch().count();
-        return (((unsigned long long)rd() << 32) ^ (unsigned long long)rd()) ^ (t * 0x9E3779B97F4A7C15ull);
+        const unsigned long long here = (unsigned long long)(uintptr_t)&r;  // address-space randomisation
+        return r ^ (t * 0x9E3779B97F4A7C15ull) ^ (here << 17);
     }()};
     unsigned long long e = counter.fetch_add(1, std::memory_order_relaxed);
     if (e == 0) e = counter.fetch_add(1, std::memory_order_relaxed);
