@@ -59,7 +59,9 @@ enum {
     FFT_EUNSUPPORTED = -2, /* valid request this library does not implement (size) */
     FFT_ENOMEM = -3,       /* device or host allocation failed */
     FFT_EALIGN = -4,       /* a pointer is not aligned to one complex element */
-    FFT_EHIP = -5          /* the HIP runtime reported an error */
+    FFT_EHIP = -5          /* the HIP runtime reported an error (or another host-side
+                              failure inside the library: no C++ exception crosses
+                              this interface) */
 };
 
 typedef struct fft_plan fft_plan; /* opaque; immutable once created */

@@ -411,15 +411,22 @@ std::map<int, void *> g_ws;
 
 }  // namespace
 
+// Every entry point that allocates host memory is a function-try-block: no
+// C++ exception leaves the C ABI (std::bad_alloc -> FFT_ENOMEM, anything
+// else -> FFT_EHIP).
 extern "C" {
 
 int fft_plan_create(int64_t n, int64_t batch, int64_t stride, int64_t dist, int storage, int dir,
-                    fft_plan **plan_out) {
+                    fft_plan **plan_out) try {
     return fft_plan_create_ex(n, batch, stride, dist, storage, dir, 0, 0u, plan_out);
+} catch (const std::bad_alloc &) {
+    return FFT_ENOMEM;
+} catch (...) {
+    return FFT_EHIP;
 }
 
 int fft_plan_create_ex(int64_t n, int64_t batch, int64_t stride, int64_t dist, int storage, int dir,
-                       int scale_log2, unsigned flags, fft_plan **plan_out) {
+                       int scale_log2, unsigned flags, fft_plan **plan_out) try {
     if (!plan_out) return FFT_EINVAL;
     if (storage != FFT_STORAGE_FP32 && storage != FFT_STORAGE_FP16) return FFT_EINVAL;
     if (dir != FFT_FORWARD && dir != FFT_INVERSE) return FFT_EINVAL;
@@ -543,6 +550,10 @@ int fft_plan_create_ex(int64_t n, int64_t batch, int64_t stride, int64_t dist, i
     p->tw = tw;
     *plan_out = p;
     return FFT_OK;
+} catch (const std::bad_alloc &) {
+    return FFT_ENOMEM;
+} catch (...) {
+    return FFT_EHIP;
 }
 
 // Three passes for n = n1 * na * nb (x viewed as n1 x n2, n2 = na * nb, j =
@@ -626,7 +637,7 @@ static int execute_column_split(const fft_plan *plan, const void *in, void *out,
     return map_hip(e);
 }
 
-int fft_execute(const fft_plan *plan, const void *in, void *out, hipStream_t stream) {
+int fft_execute(const fft_plan *plan, const void *in, void *out, hipStream_t stream) try {
     if (!plan || !in || !out) return FFT_EINVAL;
     const size_t el = plan->storage == FFT_STORAGE_FP32 ? 8 : 4;
     if (!aligned(in, el) || !aligned(out, el)) return FFT_EALIGN;
@@ -680,6 +691,10 @@ int fft_execute(const fft_plan *plan, const void *in, void *out, hipStream_t str
     }
     return map_hip(launch_fft(plan->n, plan->variant, plan->layout, plan->storage, plan->storage, inv,
                               mi355fft::EPI_NONE, in, out, plan->tw, nullptr, a, stream));
+} catch (const std::bad_alloc &) {
+    return FFT_ENOMEM;
+} catch (...) {
+    return FFT_EHIP;
 }
 
 int fft_plan_destroy(fft_plan *plan) {
@@ -926,7 +941,7 @@ int noalloc_base(int device, char **base) {
 extern "C" {
 
 int sar_form_image_ex(int64_t n_az, int64_t n_rg, int inter_storage, const void *raw, const void *range_ref,
-                      const void *az_ref, void *out, void *workspace, hipStream_t stream) {
+                      const void *az_ref, void *out, void *workspace, hipStream_t stream) try {
     if (!workspace) return FFT_EINVAL;
     int rc = sar_check(n_az, n_rg, inter_storage, raw, range_ref, az_ref, out);
     if (rc != FFT_OK) return rc;
@@ -951,10 +966,14 @@ int sar_form_image_ex(int64_t n_az, int64_t n_rg, int inter_storage, const void 
     }
     if (rc != FFT_OK) return rc;
     return sar_run(n_az, n_rg, inter_storage, raw, range_ref, az_ref, out, workspace, t, stream);
+} catch (const std::bad_alloc &) {
+    return FFT_ENOMEM;
+} catch (...) {
+    return FFT_EHIP;
 }
 
 int sar_form_image_noalloc(int64_t n_az, int64_t n_rg, int inter_storage, const void *raw, const void *range_ref,
-                           const void *az_ref, void *out, hipStream_t stream) {
+                           const void *az_ref, void *out, hipStream_t stream) try {
     int rc = sar_check(n_az, n_rg, inter_storage, raw, range_ref, az_ref, out);
     if (rc != FFT_OK) return rc;
     const size_t el = inter_storage == FFT_STORAGE_FP32 ? 8 : 4;
@@ -979,6 +998,10 @@ int sar_form_image_noalloc(int64_t n_az, int64_t n_rg, int inter_storage, const 
         t.ftab = reinterpret_cast<const float2 *>(base + na_ftab_offset(n_az));
     }
     return sar_run(n_az, n_rg, inter_storage, raw, range_ref, az_ref, out, ws, t, stream);
+} catch (const std::bad_alloc &) {
+    return FFT_ENOMEM;
+} catch (...) {
+    return FFT_EHIP;
 }
 
 size_t sar_rd_workspace_bytes(int64_t n_az, int64_t n_rg, int inter_storage) {
@@ -989,7 +1012,7 @@ size_t sar_rd_workspace_bytes(int64_t n_az, int64_t n_rg, int inter_storage) {
 }
 
 int sar_rd_form_image(int64_t n_az, int64_t n_rg, int inter_storage, const sar_geometry *geo, const void *raw,
-                      const void *range_ref, void *out, void *workspace, hipStream_t stream) {
+                      const void *range_ref, void *out, void *workspace, hipStream_t stream) try {
     if (!geo || !raw || !range_ref || !out || !workspace) return FFT_EINVAL;
     if (inter_storage != FFT_STORAGE_FP32 && inter_storage != FFT_STORAGE_FP16) return FFT_EINVAL;
     if (n_az < 1 || n_rg < 1) return FFT_EINVAL;
@@ -1081,9 +1104,13 @@ int sar_rd_form_image(int64_t n_az, int64_t n_rg, int inter_storage, const sar_g
     e = launch_fft(n_az, vrcmc, LAYOUT_RCMC, inter_storage, FFT_STORAGE_FP32, 1, EPI_RCMC, zt, out, tw_az,
                    reinterpret_cast<const float2 *>(tables), ac, stream);
     return map_hip(e);
+} catch (const std::bad_alloc &) {
+    return FFT_ENOMEM;
+} catch (...) {
+    return FFT_EHIP;
 }
 
-int sar_form_image(const void *raw, const void *range_ref, const void *az_ref, void *out, hipStream_t stream) {
+int sar_form_image(const void *raw, const void *range_ref, const void *az_ref, void *out, hipStream_t stream) try {
     if (!raw || !range_ref || !az_ref || !out) return FFT_EINVAL;
     if (fail_alloc_hook()) return FFT_ENOMEM;  // test hook: device allocation fails
     int device = 0;
@@ -1102,6 +1129,10 @@ int sar_form_image(const void *raw, const void *range_ref, const void *az_ref, v
         }
     }
     return sar_form_image_ex(4096, 4096, FFT_STORAGE_FP32, raw, range_ref, az_ref, out, ws, stream);
+} catch (const std::bad_alloc &) {
+    return FFT_ENOMEM;
+} catch (...) {
+    return FFT_EHIP;
 }
 
 const char *fft_strerror(int code) {
