@@ -188,3 +188,33 @@ def test_paper_scene_every_migration_kernel(api, paper_scene):
             assert e < TOL[inter], (v, inter, e)
             check_peaks(got[inter], ref, sc)
         v += 1
+
+
+def test_reference_spectrum_fallback_launch(api):
+    """A forced persistent row shape cannot hold the reference spectrum in the
+    range pass (the launcher answers hipErrorNotSupported), so the chain runs
+    it as a launch of its own before the pass; the image still matches the
+    oracle, and a second call on the same workspace matches the first."""
+    import os
+
+    import torch
+
+    from paper_2609_32237_amd import _lib
+
+    sc = workloads.rd_scene_small(**SMALL["square_1024"])
+    ref = oracle.rd_chain(sc.raw, sc.range_ref, sc.geometry)
+    os.environ["MI355FFT_ROW_VARIANT"] = "2"  # 1024-point rows: full exchange, persistent
+    try:
+        for inter in (0, 1):
+            log(f"rd fallback reference launch inter={inter}")
+            got = form(api, sc, inter)
+            e = rel(got.astype(np.complex128), ref)
+            assert e < TOL[inter], (inter, e)
+            raw, rref = to_dev(sc.raw), to_dev(sc.range_ref)
+            ws = torch.empty(_lib.sar_rd_workspace_bytes(1024, 1024, inter), dtype=torch.uint8, device="cuda")
+            a = api.sar_rd_form_image(raw, rref, sc.geometry, inter, workspace=ws)
+            b = api.sar_rd_form_image(raw, rref, sc.geometry, inter, workspace=ws)
+            torch.cuda.synchronize()
+            assert torch.equal(a.view(torch.float32), b.view(torch.float32))
+    finally:
+        os.environ.pop("MI355FFT_ROW_VARIANT", None)
