@@ -355,8 +355,8 @@ def breakdown(torch, api, flush, samples, copy_gbs):
 def host_info():
     """This host's CPU model, the processor count the OS reports, the CPUs this
     process may run on, and the thread count the all-core runs use: the
-    process's CPU share (OMP_NUM_THREADS when set, as on a one-GPU machine where it
-    is 16 whatever nproc says), never more than the CPUs it may run on."""
+    process's CPU share (OMP_NUM_THREADS when set: on a shared host it can be
+    smaller than what nproc reports), never more than the CPUs it may run on."""
     model = ""
     try:
         for line in open("/proc/cpuinfo"):
