@@ -180,3 +180,27 @@ def test_reference_spectra_fallback_launch(api, shape):
             check_peaks(img, ref, sc)
     finally:
         os.environ.pop("MI355FFT_ROW_VARIANT", None)
+
+
+# (the forced index also picks the azimuth reference's row shape: n_az = 4096
+# has a variant 7, 1024 a variant 6)
+@pytest.mark.parametrize("shape,variant", [((4096, 8192), 7), ((1024, 16384), 6)])
+def test_lds_twiddle_rows_in_the_range_pass(api, shape, variant):
+    """The range pass with a row shape whose second stage reads its factors from
+    LDS (twiddle mode 3), forced: its reference rows and image rows both fill
+    that table first; the image matches the oracle."""
+    import os
+
+    n_az, n_rg = shape
+    sc = workloads.sar_scene(n_az=n_az, n_rg=n_rg, n_targets=4, len_rg=256, beta_rg=0.8, len_az=96,
+                             beta_az=0.8, seed=94, min_sep=24)
+    ref = oracle.sar_chain(sc.raw, sc.range_ref, sc.az_ref)
+    os.environ["MI355FFT_ROW_VARIANT"] = str(variant)
+    try:
+        for inter in (0, 1):
+            log(f"sar {n_az}x{n_rg} row variant {variant} inter={inter}")
+            img = form(api, sc, inter)
+            assert rel(img.astype(np.complex128), ref) < TOL[inter]
+            check_peaks(img, ref, sc)
+    finally:
+        os.environ.pop("MI355FFT_ROW_VARIANT", None)
