@@ -801,8 +801,8 @@ __device__ __forceinline__ void store_remapped(float2 (&v)[K::P], void *__restri
 // An image row of a range pass whose reference spectrum workgroup 0 of the
 // same launch computes waits for it before reading the spectrum.  Workgroup 0
 // is dispatched first and waits for nothing, so the flag gets set; the bound
-// (about a second of polling) only keeps a kernel from spinning forever should
-// that ever fail.  One thread polls with agent-scope loads; the barrier then
+// (2^22 polls, a few seconds at most) only keeps a kernel from spinning
+// forever should that ever fail.  One thread polls with agent-scope loads; the barrier then
 // orders the workgroup's spectrum reads after the flag was seen.  No cache
 // can hold an older copy of the spectrum: the launch starts with L1 and L2
 // invalidated, and nothing in it reads the spectrum before it is published,
