@@ -59,7 +59,7 @@ enum { LAYOUT_ROWS = 0, LAYOUT_COLS = 1, LAYOUT_RCMC = 2, LAYOUT_ROWS_HALF = 3 }
 //                `spec` holds W_N^m for m < S followed by W_N^(S m) for
 //                m < N / S, with S = 2^aux.
 // Block -> strip maps of column kernels over the 8 XCDs (logical_block).
-enum { XCD_NONE = 0, XCD_CONTIG = 1, XCD_GROUPS = 2 };
+enum { XCD_NONE = 0, XCD_CONTIG = 1, XCD_GROUPS = 2, XCD_ROWS = 3 };
 enum {
     EPI_NONE = 0,
     EPI_MATCHED = 1,
@@ -134,7 +134,7 @@ struct KArgs {
     long long in_dist;     // elements between transform starts in the input
     long long out_dist;    // elements between transform starts in the output
     float scale;           // epilogue scale
-    int xcd_remap;         // block -> strip map over the XCDs (XCD_NONE / XCD_CONTIG / XCD_GROUPS)
+    int xcd_remap;         // block -> strip map over the XCDs (XCD_NONE / XCD_CONTIG / XCD_GROUPS / XCD_ROWS)
     int wide;              // 1: 64-bit pointer addressing (span or sign does not fit buffer offsets)
     unsigned in_span;      // bytes one workgroup's input occupies (buffer addressing)
     unsigned out_span;     // bytes one workgroup's output occupies

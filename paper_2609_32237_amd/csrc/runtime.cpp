@@ -544,9 +544,12 @@ int fft_plan_create_ex(int64_t n, int64_t batch, int64_t stride, int64_t dist, i
     p->device = device;
     p->layout = layout;
     p->variant = variant;
+    // columns: strips of a line on one XCD; rows: about 1 MiB of consecutive
+    // transforms per XCD at a time (logical_block)
     p->xcd_remap = layout == mi355fft::LAYOUT_COLS && dist == 1
                        ? strip_map(stride * (storage == FFT_STORAGE_FP32 ? 8 : 4))
-                       : mi355fft::XCD_NONE;
+                   : layout == mi355fft::LAYOUT_ROWS || layout == mi355fft::LAYOUT_ROWS_HALF ? mi355fft::XCD_ROWS
+                                                     : mi355fft::XCD_NONE;
     p->tw = tw;
     *plan_out = p;
     return FFT_OK;
