@@ -471,13 +471,16 @@ def mb_time(torch, lib, kind, src, dst, nbytes, a, b, flags, launches=20, flush=
 def copy_reference(torch):
     """The best read+write copy of 1 GiB each way on this GPU, timed like
     ``value`` (20 launches back to back): one 16-byte access per lane, plain
-    and with non-temporal loads and stores.  Returns (GB/s, details)."""
+    and with non-temporal loads and stores, each in the hardware's round-robin
+    block order and with about 1 MiB of consecutive workgroups per XCD (the
+    order the row transforms use, faster for copies too).  Returns (GB/s,
+    details)."""
     lib = membench_lib()
     nbytes = 1 << 30
     src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)
     res = {}
-    for name, flags in (("plain", 0), ("nontemporal", 3)):
+    for name, flags in (("plain", 0), ("nontemporal", 3), ("plain_xcd_groups", 4), ("nontemporal_xcd_groups", 7)):
         ms = mb_time(torch, lib, MB_COPY, src, dst, nbytes, 1, 0, flags)
         res[name] = round(2.0 * nbytes / (ms * 1e-3) / 1e9, 1)
     del src, dst
@@ -522,8 +525,15 @@ def ceilings(torch, flush):
         log(f"ceilings {mib} MiB: {row}")
         mib *= 2
     nbytes = 1 << 30
+    for name, flags in (("copy_xcd_groups", 4), ("copy_nt_xcd_groups", 7)):
+        b2b = mb_time(torch, lib, MB_COPY, src, dst, nbytes, 1, 0, flags, launches=20)
+        cold = mb_time(torch, lib, MB_COPY, src, dst, nbytes, 1, 0, flags, launches=11, flush=flush)
+        out["copy_xcd_groups"] = out.get("copy_xcd_groups", []) + [
+            {"kernel": name, "back_to_back_GB/s": round(2 * nbytes / (b2b * 1e-3) / 1e9, 1),
+             "flushed_GB/s": round(2 * nbytes / (cold * 1e-3) / 1e9, 1)}]
+        log(f"ceilings {out['copy_xcd_groups'][-1]}")
     for lds_kib in (0, 34):
-        for flags, hint in ((0, "plain"), (3, "nontemporal")):
+        for flags, hint in ((0, "plain"), (3, "nontemporal"), (4, "plain, xcd groups"), (7, "nontemporal, xcd groups")):
             b2b = mb_time(torch, lib, MB_BLOCK, src, dst, nbytes, 16, lds_kib, flags, launches=20)
             cold = mb_time(torch, lib, MB_BLOCK, src, dst, nbytes, 16, lds_kib, flags, launches=11, flush=flush)
             out["block"].append({"pattern": "32 KiB block per 256-lane workgroup, 16 x 8 B per lane",

@@ -109,7 +109,8 @@ struct Configs<2048> {
 };
 template <>
 struct Configs<4096> {
-    // measured: the hint costs about 2% on this shape, gains 2-5% on the others
+    // measured in the hardware's block order: the hint cost about 2% on this
+    // shape and gained 2-5% on the others (the default is now index 8, below)
     using Rows = KList<KCfg<4096, 16, 1, false, XCHG_FULL, 1, false, Radices<16, 16, 16>, false>,
                        KCfg<4096, 16, 1, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>,
                        KCfg<4096, 16, 1, false, XCHG_FULL, 1, true, Radices<16, 16, 16>>,
@@ -118,7 +119,9 @@ struct Configs<4096> {
                        KCfg<4096, 16, 1, false, XCHG_SPLIT, 0, false, Radices<16, 16, 16>>,
                        // every factor from the per-stage tables
                        KCfg<4096, 16, 1, false, XCHG_FULL, 2, false, Radices<16, 16, 16>, false>,
-                       KCfg<4096, 16, 1, false, XCHG_SPLIT, 2, false, Radices<16, 16, 16>>>;
+                       KCfg<4096, 16, 1, false, XCHG_SPLIT, 2, false, Radices<16, 16, 16>>,
+                       // the complex exchange with streaming row stores
+                       KCfg<4096, 16, 1, false, XCHG_FULL, 1, false, Radices<16, 16, 16>, true>>;
     using Cols = KList<KCfg<4096, 32, 4, true, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>,
                        KCfg<4096, 32, 4, true, XCHG_SPLIT, 0, false, Radices<16, 16, 16>>,
                        KCfg<4096, 16, 4, true, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>,
@@ -139,7 +142,10 @@ struct Configs<4096> {
                        KCfg<4096, 16, 4, false, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>,
                        KCfg<4096, 32, 8, false, XCHG_SPLIT, 2, false, Radices<16, 16, 16>>>;
     using RowsHalf = KList<KCfg<4096, 16, 1, false, XCHG_HALF, 1, false, Radices<16, 16, 16>>>;
-    static constexpr int kRowDefault[2] = {0, 1}, kColDefault[2] = {5, 5};
+    // FP32 rows: with the rows' XCD groups, streaming stores win back to back
+    // (6,108-6,171 against 6,015-6,027 GB/s, same process; flushed 6,120
+    // against 6,298, where a call without them leaves its write-back for later)
+    static constexpr int kRowDefault[2] = {8, 1}, kColDefault[2] = {5, 5};
     static constexpr int kRowMatched = 1, kColMatched = 5;
 };
 template <>

@@ -36,7 +36,9 @@
 //                 128-byte line run on one XCD (dispatch is round-robin over
 //                 the 8 XCDs), as the FFT's column kernels arrange.
 // flags: bit 0 non-temporal loads, bit 1 non-temporal stores (MB_COPY,
-// MB_READ, MB_WRITE, MB_BLOCK).
+// MB_READ, MB_WRITE, MB_BLOCK); bit 2 (MB_COPY in one pass, MB_BLOCK): the
+// workgroups in groups of about 1 MiB of consecutive data per XCD,
+// successive groups on successive XCDs (the FFT row kernels' block order).
 #include <hip/hip_runtime.h>
 
 #include <tuple>
@@ -82,10 +84,25 @@ __device__ __forceinline__ void st2(float2 *p, float2 v) {
 // rather than the CU's own L1.
 __device__ __forceinline__ long long rotated(int r) { return ((long long)blockIdx.x + 8LL * r) % gridDim.x; }
 
-template <bool NTL, bool NTS>
+// Block b in groups of G consecutive blocks per XCD, successive groups on
+// successive XCDs; blocks past the last whole round of 8 groups keep their
+// index.
+__device__ __forceinline__ long long grouped(long long b, long long g, long long G) {
+    const long long full = g / (8 * G) * (8 * G);
+    if (b >= full) return b;
+    const long long xcd = b & 7, local = b >> 3;
+    return ((local / G) * 8 + xcd) * G + local % G;
+}
+
+template <bool NTL, bool NTS, bool GRP = false>
 __global__ __launch_bounds__(256) void copy_kernel(const f32x4 *__restrict__ src, f32x4 *__restrict__ dst,
                                                    long long n4, int reps) {
     const long long stride = (long long)gridDim.x * 256;
+    if constexpr (GRP) {  // one pass, one 16-byte access per lane; 4 KiB workgroups, 256 per group
+        const long long i = grouped(blockIdx.x, gridDim.x, 256) * 256 + threadIdx.x;
+        if (i < n4) st4<NTS>(dst + i, ld4<NTL>(src + i));
+        return;
+    }
     for (int r = 0; r < reps; ++r)
         for (long long i = rotated(r) * 256 + threadIdx.x; i < n4; i += stride) st4<NTS>(dst + i, ld4<NTL>(src + i));
 }
@@ -111,11 +128,12 @@ __global__ __launch_bounds__(256) void write_kernel(f32x4 *__restrict__ dst, lon
 }
 
 // One block of T * P 8-byte values per workgroup: lane t loads t + T*i.
-template <int T, int P, bool NTL, bool NTS>
+template <int T, int P, bool NTL, bool NTS, bool GRP = false>
 __global__ __launch_bounds__(T) void block_kernel(const float2 *__restrict__ src, float2 *__restrict__ dst) {
     extern __shared__ float lds_pad[];  // sized by the host only to set occupancy
     if (threadIdx.x == 0xffffffffu) lds_pad[0] = 0.0f;
-    const long long base = (long long)blockIdx.x * (T * P) + threadIdx.x;
+    const long long b = GRP ? grouped(blockIdx.x, gridDim.x, (1 << 20) / (T * P * 8)) : (long long)blockIdx.x;
+    const long long base = b * (T * P) + threadIdx.x;
     float2 v[P];
 #pragma unroll
     for (int i = 0; i < P; ++i) v[i] = ld2<NTL>(src + base + T * i);
@@ -176,11 +194,15 @@ hipError_t run_block(int flags, const void *src, void *dst, long long bytes, int
     const size_t lds = (size_t)lds_kib * 1024;
     const float2 *in = static_cast<const float2 *>(src);
     float2 *out = static_cast<float2 *>(dst);
-    switch (flags & 3) {
+    switch (flags & 7) {
         case 0: return launch(block_kernel<T, P, false, false>, grid, block, lds, s, in, out);
         case 1: return launch(block_kernel<T, P, true, false>, grid, block, lds, s, in, out);
         case 2: return launch(block_kernel<T, P, false, true>, grid, block, lds, s, in, out);
-        default: return launch(block_kernel<T, P, true, true>, grid, block, lds, s, in, out);
+        case 3: return launch(block_kernel<T, P, true, true>, grid, block, lds, s, in, out);
+        case 4: return launch(block_kernel<T, P, false, false, true>, grid, block, lds, s, in, out);
+        case 5: return launch(block_kernel<T, P, true, false, true>, grid, block, lds, s, in, out);
+        case 6: return launch(block_kernel<T, P, false, true, true>, grid, block, lds, s, in, out);
+        default: return launch(block_kernel<T, P, true, true, true>, grid, block, lds, s, in, out);
     }
 }
 
@@ -233,11 +255,16 @@ int mb_run(int kind, const void *src, void *dst, long long bytes, long long a, l
         f32x4 *out = static_cast<f32x4 *>(dst);
         const int reps = (int)a;
         if (kind == MB_COPY) {
-            switch (flags & 3) {
+            if ((flags & 4) && (reps != 1 || blocks * 256 < n4)) return (int)hipErrorInvalidValue;
+            switch (flags & 7) {
                 case 0: return (int)launch(copy_kernel<false, false>, grid, block, 0, stream, in, out, n4, reps);
                 case 1: return (int)launch(copy_kernel<true, false>, grid, block, 0, stream, in, out, n4, reps);
                 case 2: return (int)launch(copy_kernel<false, true>, grid, block, 0, stream, in, out, n4, reps);
-                default: return (int)launch(copy_kernel<true, true>, grid, block, 0, stream, in, out, n4, reps);
+                case 3: return (int)launch(copy_kernel<true, true>, grid, block, 0, stream, in, out, n4, reps);
+                case 4: return (int)launch(copy_kernel<false, false, true>, grid, block, 0, stream, in, out, n4, reps);
+                case 5: return (int)launch(copy_kernel<true, false, true>, grid, block, 0, stream, in, out, n4, reps);
+                case 6: return (int)launch(copy_kernel<false, true, true>, grid, block, 0, stream, in, out, n4, reps);
+                default: return (int)launch(copy_kernel<true, true, true>, grid, block, 0, stream, in, out, n4, reps);
             }
         }
         if (kind == MB_READ) {
