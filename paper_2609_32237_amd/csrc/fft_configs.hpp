@@ -21,11 +21,12 @@ template <int N>
 struct Configs;
 
 // Each list's defaults are given per storage (FP32, FP16) for the plain
-// transform, plus one for the matched-filter (SAR) kernels: FP16 storage moves
-// half the bytes per point, so its kernels are limited by arithmetic issue and
-// prefer the higher-occupancy split exchange; the matched-filter kernels hold
-// two transforms' worth of state and prefer the shapes that do not spill.  The TWMODE 0 variants are kept
-// as regression cases for the table-read twiddle path.
+// transform and for the matched-filter (SAR) kernels (storage of the
+// intermediate): FP16 storage moves half the bytes per point, so its kernels
+// are limited by arithmetic issue and prefer the higher-occupancy split
+// exchange; the matched-filter kernels hold two transforms' worth of state and
+// prefer the shapes that do not spill.  The TWMODE 0 variants are kept as
+// regression cases for the table-read twiddle path.
 //                 N     P  C  COLS   XCHG        TW PERSIST radices
 // Short transforms serve as the column passes of four-step transforms longer
 // than 16384 points (many columns per workgroup, one or two exchanges).
@@ -36,7 +37,7 @@ struct Configs<64> {
     using Rcmc = Rows;
     using RowsHalf = Rows;
     static constexpr int kRowDefault[2] = {0, 0}, kColDefault[2] = {0, 0};
-    static constexpr int kRowMatched = 0, kColMatched = 0;
+    static constexpr int kRowMatched[2] = {0, 0}, kColMatched = 0;
 };
 template <>
 struct Configs<128> {
@@ -45,7 +46,7 @@ struct Configs<128> {
     using Rcmc = Rows;
     using RowsHalf = Rows;
     static constexpr int kRowDefault[2] = {0, 0}, kColDefault[2] = {0, 0};
-    static constexpr int kRowMatched = 0, kColMatched = 0;
+    static constexpr int kRowMatched[2] = {0, 0}, kColMatched = 0;
 };
 template <>
 struct Configs<256> {
@@ -54,7 +55,7 @@ struct Configs<256> {
     using Rcmc = Rows;
     using RowsHalf = Rows;
     static constexpr int kRowDefault[2] = {0, 0}, kColDefault[2] = {0, 0};
-    static constexpr int kRowMatched = 0, kColMatched = 0;
+    static constexpr int kRowMatched[2] = {0, 0}, kColMatched = 0;
 };
 template <>
 struct Configs<512> {
@@ -65,7 +66,7 @@ struct Configs<512> {
     using Rcmc = Rows;
     using RowsHalf = Rows;
     static constexpr int kRowDefault[2] = {0, 0}, kColDefault[2] = {0, 0};
-    static constexpr int kRowMatched = 0, kColMatched = 0;
+    static constexpr int kRowMatched[2] = {0, 0}, kColMatched = 0;
 };
 template <>
 struct Configs<1024> {
@@ -87,7 +88,7 @@ struct Configs<1024> {
                        KCfg<1024, 16, 4, false, XCHG_SPLIT, 1, false, Radices<16, 16, 4>>>;
     using RowsHalf = KList<KCfg<1024, 16, 4, false, XCHG_HALF, 1, false, Radices<16, 16, 4>>>;
     static constexpr int kRowDefault[2] = {1, 0}, kColDefault[2] = {0, 0};
-    static constexpr int kRowMatched = 1, kColMatched = 0;
+    static constexpr int kRowMatched[2] = {1, 1}, kColMatched = 0;
 };
 template <>
 struct Configs<2048> {
@@ -105,7 +106,7 @@ struct Configs<2048> {
                        KCfg<2048, 16, 8, false, XCHG_SPLIT, 1, false, Radices<16, 16, 8>>>;
     using RowsHalf = KList<KCfg<2048, 16, 2, false, XCHG_HALF, 1, false, Radices<16, 16, 8>>>;
     static constexpr int kRowDefault[2] = {0, 0}, kColDefault[2] = {0, 0};
-    static constexpr int kRowMatched = 0, kColMatched = 0;
+    static constexpr int kRowMatched[2] = {0, 0}, kColMatched = 0;
 };
 template <>
 struct Configs<4096> {
@@ -121,7 +122,9 @@ struct Configs<4096> {
                        KCfg<4096, 16, 1, false, XCHG_FULL, 2, false, Radices<16, 16, 16>, false>,
                        KCfg<4096, 16, 1, false, XCHG_SPLIT, 2, false, Radices<16, 16, 16>>,
                        // the complex exchange with streaming row stores
-                       KCfg<4096, 16, 1, false, XCHG_FULL, 1, false, Radices<16, 16, 16>, true>>;
+                       KCfg<4096, 16, 1, false, XCHG_FULL, 1, false, Radices<16, 16, 16>, true>,
+                       // the second stage's 240 factors from LDS (twiddle mode 3)
+                       KCfg<4096, 16, 1, false, XCHG_SPLIT, 3, false, Radices<16, 16, 16>>>;
     using Cols = KList<KCfg<4096, 32, 4, true, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>,
                        KCfg<4096, 32, 4, true, XCHG_SPLIT, 0, false, Radices<16, 16, 16>>,
                        KCfg<4096, 16, 4, true, XCHG_SPLIT, 1, false, Radices<16, 16, 16>>,
@@ -145,8 +148,13 @@ struct Configs<4096> {
     // FP32 rows: with the rows' XCD groups, streaming stores win back to back
     // (6,108-6,171 against 6,015-6,027 GB/s, same process; flushed 6,120
     // against 6,298, where a call without them leaves its write-back for later)
+    // matched rows with an FP16 intermediate (issue-bound): the LDS factors
+    // took the range-Doppler chain 0.4-2.8 us faster in five same-process
+    // comparisons on two boxes (181.2 -> 179.0 us on one), and moved the SAR
+    // chain by -0.4 to +1.4 us; with an FP32 intermediate they cost the SAR
+    // chain 1.6-2.7 us, so those rows keep the computed factors
     static constexpr int kRowDefault[2] = {8, 1}, kColDefault[2] = {5, 5};
-    static constexpr int kRowMatched = 1, kColMatched = 5;
+    static constexpr int kRowMatched[2] = {1, 9}, kColMatched = 5;
 };
 template <>
 struct Configs<8192> {
@@ -170,7 +178,7 @@ struct Configs<8192> {
     // the second stage's factors from LDS, 5,740 against 5,607 GB/s flushed
     // and 5,700-5,731 against 5,318-5,604 back to back (same box, one run)
     static constexpr int kRowDefault[2] = {7, 4}, kColDefault[2] = {0, 0};
-    static constexpr int kRowMatched = 0, kColMatched = 0;
+    static constexpr int kRowMatched[2] = {0, 0}, kColMatched = 0;
 };
 template <>
 struct Configs<16384> {
@@ -197,7 +205,7 @@ struct Configs<16384> {
     using RowsHalf = KList<KCfg<16384, 32, 1, false, XCHG_HALF, 1, false, Radices<32, 16, 32>>,
                            KCfg<16384, 32, 1, false, XCHG_HALF, 1, false, Radices<16, 16, 16, 4>>,
                            KCfg<16384, 16, 1, false, XCHG_HALF, 1, false, Radices<16, 16, 16, 4>>>;
-    static constexpr int kRowMatched = 4, kColMatched = 1;
+    static constexpr int kRowMatched[2] = {4, 4}, kColMatched = 1;
 };
 
 // Small batches: a batch that gives the default row shape (several
@@ -409,7 +417,7 @@ hipError_t dispatch(int variant, int layout, int in_st, int out_st, int inv, int
     const int half = (in_st | out_st) != 0;  // any FP16 storage involved
     const bool mf = epi == EPI_MATCHED || epi == EPI_MATCHED_Y;
     if (layout == LAYOUT_ROWS) {
-        int v = variant >= 0 ? variant : mf ? Configs<N>::kRowMatched : Configs<N>::kRowDefault[half];
+        int v = variant >= 0 ? variant : mf ? Configs<N>::kRowMatched[half] : Configs<N>::kRowDefault[half];
         if (variant < 0 && !mf && epi == EPI_NONE && a.batch < SmallRows<N>::below) v = SmallRows<N>::variant;
         return with_variant(v, typename Configs<N>::Rows{}, f);
     }
