@@ -37,7 +37,7 @@ struct Configs<64> {
     using Rcmc = Rows;
     using RowsHalf = Rows;
     static constexpr int kRowDefault[2] = {0, 0}, kColDefault[2] = {0, 0};
-    static constexpr int kRowMatched[2] = {0, 0}, kColMatched = 0;
+    static constexpr int kRowMatched[2] = {0, 0}, kColMatched[2] = {0, 0};
 };
 template <>
 struct Configs<128> {
@@ -46,7 +46,7 @@ struct Configs<128> {
     using Rcmc = Rows;
     using RowsHalf = Rows;
     static constexpr int kRowDefault[2] = {0, 0}, kColDefault[2] = {0, 0};
-    static constexpr int kRowMatched[2] = {0, 0}, kColMatched = 0;
+    static constexpr int kRowMatched[2] = {0, 0}, kColMatched[2] = {0, 0};
 };
 template <>
 struct Configs<256> {
@@ -55,7 +55,7 @@ struct Configs<256> {
     using Rcmc = Rows;
     using RowsHalf = Rows;
     static constexpr int kRowDefault[2] = {0, 0}, kColDefault[2] = {0, 0};
-    static constexpr int kRowMatched[2] = {0, 0}, kColMatched = 0;
+    static constexpr int kRowMatched[2] = {0, 0}, kColMatched[2] = {0, 0};
 };
 template <>
 struct Configs<512> {
@@ -66,7 +66,7 @@ struct Configs<512> {
     using Rcmc = Rows;
     using RowsHalf = Rows;
     static constexpr int kRowDefault[2] = {0, 0}, kColDefault[2] = {0, 0};
-    static constexpr int kRowMatched[2] = {0, 0}, kColMatched = 0;
+    static constexpr int kRowMatched[2] = {0, 0}, kColMatched[2] = {0, 0};
 };
 template <>
 struct Configs<1024> {
@@ -88,7 +88,7 @@ struct Configs<1024> {
                        KCfg<1024, 16, 4, false, XCHG_SPLIT, 1, false, Radices<16, 16, 4>>>;
     using RowsHalf = KList<KCfg<1024, 16, 4, false, XCHG_HALF, 1, false, Radices<16, 16, 4>>>;
     static constexpr int kRowDefault[2] = {1, 0}, kColDefault[2] = {0, 0};
-    static constexpr int kRowMatched[2] = {1, 1}, kColMatched = 0;
+    static constexpr int kRowMatched[2] = {1, 1}, kColMatched[2] = {0, 0};
 };
 template <>
 struct Configs<2048> {
@@ -106,7 +106,7 @@ struct Configs<2048> {
                        KCfg<2048, 16, 8, false, XCHG_SPLIT, 1, false, Radices<16, 16, 8>>>;
     using RowsHalf = KList<KCfg<2048, 16, 2, false, XCHG_HALF, 1, false, Radices<16, 16, 8>>>;
     static constexpr int kRowDefault[2] = {0, 0}, kColDefault[2] = {0, 0};
-    static constexpr int kRowMatched[2] = {0, 0}, kColMatched = 0;
+    static constexpr int kRowMatched[2] = {0, 0}, kColMatched[2] = {0, 0};
 };
 template <>
 struct Configs<4096> {
@@ -153,8 +153,13 @@ struct Configs<4096> {
     // comparisons on two boxes (181.2 -> 179.0 us on one), and moved the SAR
     // chain by -0.4 to +1.4 us; with an FP32 intermediate they cost the SAR
     // chain 1.6-2.7 us, so those rows keep the computed factors
+    // matched columns (the SAR azimuth pass) reading an FP32 intermediate:
+    // the 4-column strips, two workgroups per CU, took the chain from
+    // 140.9 to 134.8-134.9 us (same process, two runs); with an FP16
+    // intermediate (16-byte pieces) they measured 125.5-126.3 against
+    // 125.2-126.0 us, so those keep the 8-column strips
     static constexpr int kRowDefault[2] = {8, 1}, kColDefault[2] = {5, 5};
-    static constexpr int kRowMatched[2] = {1, 9}, kColMatched = 5;
+    static constexpr int kRowMatched[2] = {1, 9}, kColMatched[2] = {6, 5};
 };
 template <>
 struct Configs<8192> {
@@ -178,7 +183,7 @@ struct Configs<8192> {
     // the second stage's factors from LDS, 5,740 against 5,607 GB/s flushed
     // and 5,700-5,731 against 5,318-5,604 back to back (same box, one run)
     static constexpr int kRowDefault[2] = {7, 4}, kColDefault[2] = {0, 0};
-    static constexpr int kRowMatched[2] = {0, 0}, kColMatched = 0;
+    static constexpr int kRowMatched[2] = {0, 0}, kColMatched[2] = {0, 0};
 };
 template <>
 struct Configs<16384> {
@@ -205,7 +210,7 @@ struct Configs<16384> {
     using RowsHalf = KList<KCfg<16384, 32, 1, false, XCHG_HALF, 1, false, Radices<32, 16, 32>>,
                            KCfg<16384, 32, 1, false, XCHG_HALF, 1, false, Radices<16, 16, 16, 4>>,
                            KCfg<16384, 16, 1, false, XCHG_HALF, 1, false, Radices<16, 16, 16, 4>>>;
-    static constexpr int kRowMatched[2] = {4, 4}, kColMatched = 1;
+    static constexpr int kRowMatched[2] = {4, 4}, kColMatched[2] = {1, 1};
 };
 
 // Small batches: a batch that gives the default row shape (several
@@ -246,7 +251,7 @@ struct KAt<I, KList<K, Ks...>> {
 template <int N>
 struct FourStepCols {
     static constexpr int plain[2] = {Configs<N>::kColDefault[0], Configs<N>::kColDefault[1]};
-    static constexpr int matched = Configs<N>::kColMatched;
+    static constexpr int matched = Configs<N>::kColMatched[0];  // (FP32 data only)
 };
 template <>
 struct FourStepCols<4096> {
@@ -434,7 +439,7 @@ hipError_t dispatch(int variant, int layout, int in_st, int out_st, int inv, int
         } else if (epi == EPI_SCALE) {
             v = ScaleCols<N>::v[half];
         } else {
-            v = mf ? Configs<N>::kColMatched : Configs<N>::kColDefault[half];
+            v = mf ? Configs<N>::kColMatched[half] : Configs<N>::kColDefault[half];
         }
     }
     return with_variant(v, Cols{}, f);
