@@ -96,7 +96,8 @@ def test_fixed_size_entry_point_matches_ex(api, scene):
     assert torch.equal(out1.view(torch.float32), out3.view(torch.float32))
 
 
-@pytest.mark.parametrize("shape", [(1024, 2048), (2048, 1024), (1024, 1024), (16384, 1024), (1024, 16384), (8192, 1024)])
+@pytest.mark.parametrize("shape", [(1024, 2048), (2048, 1024), (1024, 1024), (16384, 1024), (1024, 16384), (8192, 1024),
+                                   (4096, 1024), (4096, 2048), (2048, 4096)])
 @pytest.mark.parametrize("inter", [0, 1])
 def test_other_shapes(api, shape, inter):
     n_az, n_rg = shape
